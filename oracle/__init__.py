@@ -1,0 +1,211 @@
+"""COVER fp64 CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The HIP library and its Python binding never
+call it; the two share no code.
+
+The arithmetic lives in ``cover_oracle.c`` (plain C, fp64, built with
+``-ffp-contract=off`` so no multiply-add is fused).  This module only marshals numpy
+arrays in and out through ctypes.  Paper: arXiv 2602.06161.
+
+Functions (each cites the passage it follows):
+  attn              Sec. 5.1 + App. B.1, materialised leave-one-out view per row
+  attn_closed_form  App. B.2-B.4, the paper's post-hoc diagonal correction
+  select            Sec. 5.3, score / adaptive budget / exclusion / top-k
+  token_stats       Sec. 5.3 u(j) and Sec. 3 confidence, from logits
+  attn_stats        Sec. 5.3 d_in / d_out from the head-averaged attention
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cover_oracle.c")
+_LIB = os.path.join(_HERE, "libcover_oracle.so")
+_CFLAGS = ["-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared"]
+
+_ERRORS = {1: "invalid sizes", 2: "seed contract violated (out of range or duplicate)",
+           3: "non-finite or negative selection input", 4: "allocation failure"}
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (host only)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", *_CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        I64 = ctypes.c_int64
+        D = ctypes.c_double
+        lib.cover_oracle_attn.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, D, I, P, I64, P, P]
+        lib.cover_oracle_attn_closed.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, D, P, P]
+        lib.cover_oracle_select.argtypes = [P, P, P, P, I, I, I, I, P, P, P]
+        lib.cover_oracle_token_stats.argtypes = [P, P, I64, I64, P, P, P]
+        lib.cover_oracle_attn_stats.argtypes = [P, P, P, P, P, I, I, I, I, I, I, D, I, I, P, P, P, P]
+        for f in (lib.cover_oracle_attn, lib.cover_oracle_attn_closed, lib.cover_oracle_select,
+                  lib.cover_oracle_token_stats, lib.cover_oracle_attn_stats):
+            f.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _f64(x) -> np.ndarray:
+    """Exact widening of any stored float (bf16, fp16, fp32, fp64) to a contiguous fp64 array."""
+    if hasattr(x, "detach"):  # a torch tensor: widen on the host
+        x = x.detach().to("cpu").double().numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _i32(x) -> np.ndarray:
+    if hasattr(x, "detach"):
+        x = x.detach().to("cpu").numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))
+
+
+def _attn_args(q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed, scale):
+    q, kl, vl, kc, vc = (_f64(t) for t in (q, k_live, v_live, k_cache, v_cache))
+    if q.ndim != 4 or kl.ndim != 4:
+        raise ValueError("q is [B,Hq,L,d] and k/v are [B,Hkv,L,d]")
+    B, Hq, L, d = q.shape
+    Hkv = kl.shape[1]
+    for t in (kl, vl, kc, vc):
+        if t.shape != (B, Hkv, L, d):
+            raise ValueError(f"k/v shape {t.shape} != {(B, Hkv, L, d)}")
+    si = _i32(seed_idx).reshape(B, -1) if seed_idx is not None else np.zeros((B, 0), np.int32)
+    ns = _i32(n_seed).reshape(B) if n_seed is not None else np.zeros((B,), np.int32)
+    si = np.ascontiguousarray(si)
+    if scale is None or scale == 0.0:
+        scale = 1.0 / np.sqrt(d)
+    return q, kl, vl, kc, vc, si, ns, (B, Hq, Hkv, L, d, si.shape[1]), float(scale)
+
+
+def attn(q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed, scale=None, mode="literal",
+         rows=None):
+    """Leave-one-out COVER attention (Sec. 5.1, App. B.1), fp64.
+
+    Returns (out, lse).  With rows=None: out [B,Hq,L,d], lse [B,Hq,L].  With rows (flat
+    indices (b*Hq+h)*L+i): out [n,d], lse [n].  mode: "literal" (a materialised L x d view
+    per row) or "fast" (shared override view for non-seed rows; bitwise identical).
+    """
+    q, kl, vl, kc, vc, si, ns, dims, scale = _attn_args(q, k_live, v_live, k_cache, v_cache,
+                                                        seed_idx, n_seed, scale)
+    B, Hq, Hkv, L, d, ms = dims
+    if rows is None:
+        out = np.zeros((B, Hq, L, d))
+        lse = np.zeros((B, Hq, L))
+        rp, nr = None, 0
+    else:
+        rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64).reshape(-1))
+        out = np.zeros((rows.size, d))
+        lse = np.zeros((rows.size,))
+        rp, nr = _ptr(rows), rows.size
+    rc = _load().cover_oracle_attn(_ptr(q), _ptr(kl), _ptr(vl), _ptr(kc), _ptr(vc), _ptr(si),
+                                   _ptr(ns), B, Hq, Hkv, L, d, ms, scale,
+                                   1 if mode == "literal" else 0, rp, nr, _ptr(out), _ptr(lse))
+    _check(rc)
+    return out, lse
+
+
+def attn_closed_form(q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed, scale=None):
+    """Override attention + the paper's closed-form diagonal correction (App. B.2-B.4)."""
+    q, kl, vl, kc, vc, si, ns, dims, scale = _attn_args(q, k_live, v_live, k_cache, v_cache,
+                                                        seed_idx, n_seed, scale)
+    B, Hq, Hkv, L, d, ms = dims
+    out = np.zeros((B, Hq, L, d))
+    lse = np.zeros((B, Hq, L))
+    rc = _load().cover_oracle_attn_closed(_ptr(q), _ptr(kl), _ptr(vl), _ptr(kc), _ptr(vc),
+                                          _ptr(si), _ptr(ns), B, Hq, Hkv, L, d, ms, scale,
+                                          _ptr(out), _ptr(lse))
+    _check(rc)
+    return out, lse
+
+
+def select(logp, d_in, d_out, flags, max_seeds, pos_offset=0):
+    """Stability-aware seed selection with adaptive budget (Sec. 5.3).
+
+    Inputs are fp32 [B,Lr] (logp, d_in, d_out) and uint8 flags [B,Lr] (bit0: unmasked,
+    bit1: excluded).  Returns (seed_idx int32 [B,max_seeds] ascending, -1 padded;
+    n_seed int32 [B]; score fp64 [B,Lr]).
+    """
+    def f32(x):
+        if hasattr(x, "detach"):
+            x = x.detach().to("cpu").numpy()
+        return np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    lp, di, do = f32(logp), f32(d_in), f32(d_out)
+    if lp.ndim == 1:
+        lp, di, do = lp[None], di[None], do[None]
+    fl = flags.detach().to("cpu").numpy() if hasattr(flags, "detach") else flags
+    fl = np.ascontiguousarray(np.asarray(fl, dtype=np.uint8)).reshape(lp.shape)
+    B, Lr = lp.shape
+    seed_idx = np.full((B, max_seeds), -1, np.int32)
+    n_seed = np.zeros((B,), np.int32)
+    score = np.zeros((B, Lr))
+    rc = _load().cover_oracle_select(_ptr(lp), _ptr(di), _ptr(do), _ptr(fl), B, Lr,
+                                     int(max_seeds), int(pos_offset), _ptr(seed_idx),
+                                     _ptr(n_seed), _ptr(score))
+    _check(rc)
+    return seed_idx, n_seed, score
+
+
+def token_stats(logits, y):
+    """Per row: log p(y), max probability, argmax (Sec. 5.3 u(j); Sec. 3 confidence)."""
+    x = _f64(logits)
+    R, V = x.shape
+    yy = _i32(y).reshape(R)
+    logp = np.zeros(R)
+    conf = np.zeros(R)
+    amax = np.zeros(R, np.int32)
+    rc = _load().cover_oracle_token_stats(_ptr(x), _ptr(yy), R, V, _ptr(logp), _ptr(conf),
+                                          _ptr(amax))
+    _check(rc)
+    return logp, conf, amax
+
+
+def attn_stats(q, k_live, k_cache, seed_idx, n_seed, r0, masked, drafted, scale=None):
+    """d_in / d_out over the region [r0, r0+Lr) from head-averaged corrected weights (Sec. 5.3)."""
+    qq, kl, kc = _f64(q), _f64(k_live), _f64(k_cache)
+    B, Hq, L, d = qq.shape
+    Hkv = kl.shape[1]
+    si = np.ascontiguousarray(_i32(seed_idx).reshape(B, -1))
+    ns = _i32(n_seed).reshape(B)
+    m = np.ascontiguousarray(np.asarray(masked, dtype=np.uint8)).reshape(B, -1)
+    dr = np.ascontiguousarray(np.asarray(drafted, dtype=np.uint8)).reshape(B, -1)
+    Lr = m.shape[1]
+    if scale is None or scale == 0.0:
+        scale = 1.0 / np.sqrt(d)
+    d_in = np.zeros((B, Lr))
+    d_out = np.zeros((B, Lr))
+    rc = _load().cover_oracle_attn_stats(_ptr(qq), _ptr(kl), _ptr(kc), _ptr(si), _ptr(ns), B, Hq,
+                                         Hkv, L, d, si.shape[1], float(scale), int(r0), Lr,
+                                         _ptr(m), _ptr(dr), _ptr(d_in), _ptr(d_out))
+    _check(rc)
+    return d_in, d_out
