@@ -1,0 +1,164 @@
+/*
+ * cover.h -- C ABI of the COVER hot path on MI355X (gfx950).
+ *
+ * COVER (arXiv 2602.06161) verifies previously unmasked "seed" positions inside the same
+ * forward pass that drafts new tokens.  This library provides the two per-step device
+ * operations of that pass:
+ *
+ *   cover_attn_fwd      bidirectional attention over the KV-cache-overridden memory with the
+ *                       diagonal correction for seed rows (Sec. 5.1; App. B).
+ *   cover_select_seeds  stability-aware seed scoring, adaptive budget and top-k
+ *                       (Sec. 5.3).
+ *
+ * Conventions shared by every entry point
+ *   - Every data pointer is device memory owned by the caller (hipMalloc, or a framework
+ *     allocator).  The library allocates nothing, frees nothing and never synchronises;
+ *     work is enqueued on `stream` (0 = the null stream) and runs asynchronously.
+ *   - Descriptor and pointer errors are detected on the host before anything is enqueued:
+ *     the call then returns COVER_ERR_INVALID or COVER_ERR_UNSUPPORTED and writes nothing.
+ *   - COVER_ERR_HIP means the HIP runtime rejected the launch.
+ *   - Device-resident arguments (seed lists, seed counts, selection inputs) are not
+ *     validated; their contract is stated per function.  Violations give unspecified
+ *     results but never out-of-bounds memory accesses.
+ *   - Outputs must not alias inputs.
+ */
+#ifndef COVER_H
+#define COVER_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COVER_OK = 0,
+  COVER_ERR_INVALID = -1,     /* bad pointer, size, stride or alignment            */
+  COVER_ERR_UNSUPPORTED = -2, /* valid request outside what the kernels implement  */
+  COVER_ERR_HIP = -3          /* the HIP runtime reported an error at launch       */
+} cover_status;
+
+typedef enum { COVER_F32 = 0, COVER_BF16 = 1 } cover_dtype;
+
+/* Largest sequence length the attention kernels accept (the seed bitmap of a sequence is
+ * staged in on-chip memory). */
+#define COVER_MAX_L 65536
+/* Largest selection region per batch row. */
+#define COVER_MAX_LR 16384
+
+/*
+ * Attention problem description.
+ *   B        batch rows (>= 0; 0 is a no-op)
+ *   Hq, Hkv  query heads and key/value heads; Hq % Hkv == 0; query head h reads key/value
+ *            head h / (Hq / Hkv) (grouped-query attention; Hq == Hkv is plain multi-head)
+ *   L        sequence length, prompt plus response (0 is a no-op; <= COVER_MAX_L)
+ *   d        head dimension: 64 or 128
+ *   max_seeds  row stride of seed_idx (>= 0)
+ *   dtype    element type of q, k_live, v_live, k_cache, v_cache and out
+ *   scale    score scale; 0 selects 1/sqrt(d) (Sec. 5.1)
+ *   q_sb, q_sh, q_sl     element strides of q and out over (batch, head, position)
+ *   kv_sb, kv_sh, kv_sl  element strides shared by k_live, v_live, k_cache, v_cache
+ * The head dimension is contiguous (stride 1).  Base pointers must be 16-byte aligned and
+ * every stride a multiple of 16 bytes' worth of elements.
+ */
+typedef struct {
+  int32_t B, Hq, Hkv, L, d;
+  int32_t max_seeds;
+  cover_dtype dtype;
+  float scale;
+  int64_t q_sb, q_sh, q_sl;
+  int64_t kv_sb, kv_sh, kv_sl;
+} cover_attn_desc;
+
+/*
+ * cover_attn_fwd -- COVER attention of one layer (Sec. 5.1 "KV cache override" and
+ * "diagonal correction"; App. B.1-B.4).
+ *
+ * For batch row b with seed set S_b = { seed_idx[b, t] : 0 <= t < n_seed[b] }, query head h
+ * and key/value head g:
+ *   override memory   K'_j = k_cache[b,g,j] if j in S_b, else k_live[b,g,j]; V' likewise
+ *   row view          K^(i) = K', except K^(i)_i = k_live[b,g,i] when i in S_b (the key of
+ *                     the masked input); V^(i) likewise
+ *   out[b,h,i,:]      = sum_j softmax_j(scale * <q_i, K^(i)_j>) V^(i)_j
+ *   lse[b,h,i]        = log sum_j exp(scale * <q_i, K^(i)_j>)   (natural log)
+ * Non-seed rows therefore attend to the overridden memory unchanged, and each seed row sees
+ * cached states everywhere except its own diagonal, which is the leave-one-out view the
+ * paper's closed-form correction (App. B.4) produces.  All scores are kept in fp32 and the
+ * softmax is taken over all L positions (non-causal).
+ *
+ * Arguments
+ *   q        [B,Hq,L,d]   queries of the verification input (seeds masked)
+ *   k_live, v_live   [B,Hkv,L,d]  keys/values of the verification input
+ *   k_cache, v_cache [B,Hkv,L,d]  keys/values cached from the previous step, indexed by
+ *                     absolute position; only rows at seed positions are read
+ *   seed_idx [B,max_seeds] int32  seed positions; may be NULL when max_seeds == 0
+ *   n_seed   [B] int32            seeds per batch row; may be NULL when max_seeds == 0
+ *   out      [B,Hq,L,d]   output, same dtype and strides as q
+ *   lse      [B,Hq,L] fp32, contiguous; may be NULL
+ *   desc     problem description (host memory)
+ * Device-data contract: 0 <= n_seed[b] <= max_seeds; seed_idx[b,0..n_seed[b]) distinct and in
+ * [0, L) (any order).  n_seed outside [0, max_seeds] is clamped into it and entries outside
+ * [0, L) are ignored.
+ * Returns COVER_ERR_UNSUPPORTED for d not in {64, 128} or L > COVER_MAX_L.
+ */
+cover_status cover_attn_fwd(const void* q, const void* k_live, const void* v_live,
+                            const void* k_cache, const void* v_cache,
+                            const int32_t* seed_idx, const int32_t* n_seed,
+                            void* out, float* lse,
+                            const cover_attn_desc* desc, hipStream_t stream);
+
+/*
+ * Selection description.
+ *   B           batch rows (>= 0)
+ *   Lr          candidate region length per row (>= 0, <= COVER_MAX_LR)
+ *   max_seeds   row stride / capacity of seed_idx (>= 0)
+ *   pos_offset  added to every emitted position (the region's start in the sequence)
+ */
+typedef struct {
+  int32_t B, Lr;
+  int32_t max_seeds;
+  int32_t pos_offset;
+} cover_select_desc;
+
+/*
+ * cover_select_seeds -- stability-aware seed selection with an adaptive revision rate
+ * (Sec. 5.3 "Stability aware seed scoring", "Adaptive revision rate").
+ *
+ * Per batch row, over region positions j in [0, Lr):
+ *   flags bit 0 = j is unmasked (j in U_t); bit 1 = j is excluded (a seed of the previous
+ *   step, or its ReMask budget is used up); other bits are ignored.
+ *   score s_j   = ((-(double)logp_j) * (1 + (double)d_in_j)) / (1 + (double)d_out_j), for j
+ *                 in U_t, in IEEE fp64 with round-to-nearest and this exact association
+ *   mean        = (sum of s_j over U_t) / |U_t|, the sum taken as a stride-halving tree over
+ *                 the region zero-padded to the next power of two
+ *   budget      = least k >= 0 with k*k >= c, c = #{ j in U_t : s_j > mean } (= n_t pi_t)
+ *   selection   = the min(budget, #eligible, max_seeds) eligible positions (in U_t, not
+ *                 excluded) ranked first by score descending then position ascending
+ * Outputs
+ *   seed_idx [B,max_seeds] int32: selected positions + pos_offset in ascending order,
+ *            then -1; n_seed [B] int32: how many; score [B,Lr] fp64 (may be NULL): s_j on
+ *            U_t, 0 elsewhere.  The results are bit-exact functions of the inputs.
+ * Inputs: logp, d_in, d_out fp32 [B,Lr] row-major (logp = log p_j(y_j) <= 0, the model's
+ * log-probability of the token currently at j; d_in, d_out >= 0 are the in/out attention
+ * masses); flags uint8 [B,Lr].  Inputs at positions outside U_t are not read.  Device-data
+ * contract: values on U_t finite, d_in and d_out >= 0.
+ * The output layout matches cover_attn_fwd's seed_idx / n_seed, so the next step's
+ * attention can consume it without a host round-trip.
+ */
+cover_status cover_select_seeds(const float* logp, const float* d_in, const float* d_out,
+                                const uint8_t* flags,
+                                int32_t* seed_idx, int32_t* n_seed, double* score,
+                                const cover_select_desc* desc, hipStream_t stream);
+
+/* Static string naming a status code. */
+const char* cover_status_str(cover_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t cover_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COVER_H */

@@ -1,0 +1,161 @@
+"""ctypes binding of the COVER C ABI (``include/cover.h``).
+
+Argument marshalling only: torch supplies device memory and the stream; every step of the
+computation runs in the HIP kernels of ``libcover.so``.  There is no fallback -- if the
+library has not been built, or a call is rejected, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+from .build import LIB
+
+COVER_OK, COVER_ERR_INVALID, COVER_ERR_UNSUPPORTED, COVER_ERR_HIP = 0, -1, -2, -3
+COVER_F32, COVER_BF16 = 0, 1
+COVER_MAX_L = 65536
+COVER_MAX_LR = 16384
+
+EXPORTED = ("cover_attn_fwd", "cover_select_seeds", "cover_status_str", "cover_version")
+
+
+class CoverError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_str(status)} ({status})")
+        self.status = status
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
+                ("L", ctypes.c_int32), ("d", ctypes.c_int32), ("max_seeds", ctypes.c_int32),
+                ("dtype", ctypes.c_int), ("scale", ctypes.c_float),
+                ("q_sb", ctypes.c_int64), ("q_sh", ctypes.c_int64), ("q_sl", ctypes.c_int64),
+                ("kv_sb", ctypes.c_int64), ("kv_sh", ctypes.c_int64), ("kv_sl", ctypes.c_int64)]
+
+
+class SelectDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("Lr", ctypes.c_int32), ("max_seeds", ctypes.c_int32),
+                ("pos_offset", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libcover.so (built in-tree); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError(f"COVER HIP library not built ({LIB}); run "
+                               "`python -m paper_2602_06161_amd.build` or __graft_entry__.build()")
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        L.cover_attn_fwd.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.POINTER(AttnDesc), P]
+        L.cover_attn_fwd.restype = ctypes.c_int
+        L.cover_select_seeds.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(SelectDesc), P]
+        L.cover_select_seeds.restype = ctypes.c_int
+        L.cover_status_str.argtypes = [ctypes.c_int]
+        L.cover_status_str.restype = ctypes.c_char_p
+        L.cover_version.argtypes = []
+        L.cover_version.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def status_str(s: int) -> str:
+    return lib().cover_status_str(s).decode()
+
+
+def version() -> int:
+    return lib().cover_version()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def attn_desc(q: torch.Tensor, k: torch.Tensor, max_seeds: int, scale: float = 0.0) -> AttnDesc:
+    B, Hq, L, d = q.shape
+    Hkv = k.shape[1]
+    dt = {torch.float32: COVER_F32, torch.bfloat16: COVER_BF16}.get(q.dtype)
+    if dt is None:
+        raise TypeError(f"unsupported dtype {q.dtype}")
+    return AttnDesc(B, Hq, Hkv, L, d, max_seeds, dt, float(scale),
+                    q.stride(0), q.stride(1), q.stride(2), k.stride(0), k.stride(1), k.stride(2))
+
+
+def cover_attn_fwd(q, k_live, v_live, k_cache, v_cache, seed_idx=None, n_seed=None, out=None,
+                   lse=None, scale: float = 0.0, stream=None, want_lse: bool = True):
+    """COVER attention of one layer.  Tensors on the GPU: q [B,Hq,L,d]; k/v [B,Hkv,L,d]
+    (head dim contiguous, all four K/V tensors with identical strides); seed_idx int32
+    [B,max_seeds]; n_seed int32 [B].  Returns (out, lse)."""
+    for t in (k_live, v_live, k_cache, v_cache):
+        if t.shape != k_live.shape or t.stride() != k_live.stride() or t.dtype != q.dtype:
+            raise ValueError("k_live, v_live, k_cache, v_cache need equal shape, strides and dtype")
+    if q.stride(-1) != 1 or k_live.stride(-1) != 1:
+        raise ValueError("head dimension must be contiguous")
+    max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+    if seed_idx is not None and (seed_idx.dtype != torch.int32 or n_seed is None
+                                 or n_seed.dtype != torch.int32 or not seed_idx.is_contiguous()):
+        raise ValueError("seed_idx and n_seed must be contiguous int32 tensors")
+    B, Hq, L, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if out.shape != q.shape or out.stride() != q.stride() or out.dtype != q.dtype:
+        raise ValueError("out must match q's shape, strides and dtype")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, L), device=q.device, dtype=torch.float32)
+    desc = attn_desc(q, k_live, max_seeds, scale)
+    st = lib().cover_attn_fwd(_ptr(q), _ptr(k_live), _ptr(v_live), _ptr(k_cache), _ptr(v_cache),
+                              _ptr(seed_idx), _ptr(n_seed), _ptr(out), _ptr(lse),
+                              ctypes.byref(desc), _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_attn_fwd")
+    return out, lse
+
+
+def cover_select_seeds(logp, d_in, d_out, flags, max_seeds: int, pos_offset: int = 0,
+                       seed_idx=None, n_seed=None, score=None, want_score: bool = True,
+                       stream=None):
+    """Stability-aware seed selection.  logp/d_in/d_out fp32 [B,Lr], flags uint8 [B,Lr] on the
+    GPU (contiguous).  Returns (seed_idx int32 [B,max_seeds], n_seed int32 [B], score fp64
+    [B,Lr] or None)."""
+    B, Lr = logp.shape
+    for t, dt in ((logp, torch.float32), (d_in, torch.float32), (d_out, torch.float32),
+                  (flags, torch.uint8)):
+        if t.shape != (B, Lr) or t.dtype != dt or not t.is_contiguous():
+            raise ValueError("selection inputs must be contiguous [B,Lr] (fp32 x3, uint8 flags)")
+    dev = logp.device
+    if seed_idx is None:
+        seed_idx = torch.empty((B, max_seeds), device=dev, dtype=torch.int32)
+    if n_seed is None:
+        n_seed = torch.empty((B,), device=dev, dtype=torch.int32)
+    if score is None and want_score:
+        score = torch.empty((B, Lr), device=dev, dtype=torch.float64)
+    desc = SelectDesc(B, Lr, max_seeds, pos_offset)
+    st = lib().cover_select_seeds(_ptr(logp), _ptr(d_in), _ptr(d_out), _ptr(flags),
+                                  _ptr(seed_idx), _ptr(n_seed), _ptr(score), ctypes.byref(desc),
+                                  _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_select_seeds")
+    return seed_idx, n_seed, score
+
+
+def attn_flops(B: int, Hq: int, L: int, d: int) -> int:
+    """Algorithmic flops of one call: QK^T plus PV, 2 flops per multiply-add, non-causal."""
+    return 4 * B * Hq * L * L * d
+
+
+def default_scale(d: int) -> float:
+    return 1.0 / math.sqrt(d)

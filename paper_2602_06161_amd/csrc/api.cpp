@@ -1,0 +1,104 @@
+// C ABI of the COVER library: host-side validation, then one kernel launch per call.
+// Every check here runs before anything is enqueued, so a rejected call writes nothing.
+#include <math.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+cover_status hip_status(hipError_t e) { return e == hipSuccess ? COVER_OK : COVER_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* cover_status_str(cover_status s) {
+  switch (s) {
+    case COVER_OK: return "COVER_OK";
+    case COVER_ERR_INVALID: return "COVER_ERR_INVALID";
+    case COVER_ERR_UNSUPPORTED: return "COVER_ERR_UNSUPPORTED";
+    case COVER_ERR_HIP: return "COVER_ERR_HIP";
+  }
+  return "COVER_ERR_UNKNOWN";
+}
+
+int32_t cover_version(void) { return 100; }  // 0.1.0
+
+cover_status cover_attn_fwd(const void* q, const void* k_live, const void* v_live,
+                            const void* k_cache, const void* v_cache,
+                            const int32_t* seed_idx, const int32_t* n_seed,
+                            void* out, float* lse,
+                            const cover_attn_desc* desc, hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_attn_desc& D = *desc;
+  if (D.B < 0 || D.L < 0 || D.Hq < 1 || D.Hkv < 1 || D.d < 1 || D.max_seeds < 0)
+    return COVER_ERR_INVALID;
+  if (D.Hq % D.Hkv != 0) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_F32 && D.dtype != COVER_BF16) return COVER_ERR_INVALID;
+  if (!(D.scale >= 0.0f) || isinf(D.scale)) return COVER_ERR_INVALID;  // rejects NaN too
+  if (D.d != 64 && D.d != 128) return COVER_ERR_UNSUPPORTED;
+  if (D.L > COVER_MAX_L) return COVER_ERR_UNSUPPORTED;
+  if (D.B == 0 || D.L == 0) return COVER_OK;
+
+  const int64_t esz = D.dtype == COVER_BF16 ? 2 : 4;
+  const int64_t vec = 16 / esz;  // elements per 16-byte chunk
+  const void* tensors[6] = {q, k_live, v_live, k_cache, v_cache, out};
+  for (const void* t : tensors)
+    if (!t || !aligned(t, 16)) return COVER_ERR_INVALID;
+  const int64_t strides[6] = {D.q_sb, D.q_sh, D.q_sl, D.kv_sb, D.kv_sh, D.kv_sl};
+  for (int64_t s : strides)
+    if (s < 0 || s % vec != 0) return COVER_ERR_INVALID;
+  if (D.L > 1 && (D.q_sl < D.d || D.kv_sl < D.d)) return COVER_ERR_INVALID;
+  if (D.max_seeds > 0) {
+    if (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4))
+      return COVER_ERR_INVALID;
+  }
+  if (lse && !aligned(lse, 4)) return COVER_ERR_INVALID;
+  const int64_t qtile = D.dtype == COVER_BF16 ? 128 : 64;
+  if ((int64_t)D.B * D.Hq * ((D.L + qtile - 1) / qtile) > 0x7fffffffLL) return COVER_ERR_UNSUPPORTED;
+
+  cover::AttnArgs a;
+  a.q = q; a.k_live = k_live; a.v_live = v_live; a.k_cache = k_cache; a.v_cache = v_cache;
+  a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
+  a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
+  a.out = out; a.lse = lse;
+  a.B = D.B; a.Hq = D.Hq; a.Hkv = D.Hkv; a.L = D.L; a.d = D.d; a.max_seeds = D.max_seeds;
+  a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
+  a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
+  a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  return hip_status(D.dtype == COVER_BF16 ? cover::launch_attn_bf16(a, stream)
+                                          : cover::launch_attn_f32(a, stream));
+}
+
+cover_status cover_select_seeds(const float* logp, const float* d_in, const float* d_out,
+                                const uint8_t* flags,
+                                int32_t* seed_idx, int32_t* n_seed, double* score,
+                                const cover_select_desc* desc, hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_select_desc& D = *desc;
+  if (D.B < 0 || D.Lr < 0 || D.max_seeds < 0) return COVER_ERR_INVALID;
+  if (D.Lr > COVER_MAX_LR) return COVER_ERR_UNSUPPORTED;
+  if (D.B == 0) return COVER_OK;
+  if (!n_seed || !aligned(n_seed, 4)) return COVER_ERR_INVALID;
+  if (D.max_seeds > 0 && (!seed_idx || !aligned(seed_idx, 4))) return COVER_ERR_INVALID;
+  if (D.Lr > 0) {
+    if (!logp || !d_in || !d_out || !flags) return COVER_ERR_INVALID;
+    if (!aligned(logp, 4) || !aligned(d_in, 4) || !aligned(d_out, 4)) return COVER_ERR_INVALID;
+  }
+  if (score && !aligned(score, 8)) return COVER_ERR_INVALID;
+  // emitted positions must stay representable
+  if ((int64_t)D.pos_offset + D.Lr > 0x7fffffffLL || (int64_t)D.pos_offset < -0x7fffffffLL)
+    return COVER_ERR_INVALID;
+
+  cover::SelectArgs a;
+  a.logp = logp; a.d_in = d_in; a.d_out = d_out; a.flags = flags;
+  a.seed_idx = seed_idx; a.n_seed = n_seed; a.score = score;
+  a.B = D.B; a.Lr = D.Lr; a.max_seeds = D.max_seeds; a.pos_offset = D.pos_offset;
+  return hip_status(cover::launch_select(a, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,39 @@
+// Internal launch interface between the C ABI (api.cpp) and the HIP kernels.
+// Host-validated arguments only: every entry here assumes the descriptor checks passed.
+#pragma once
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+namespace cover {
+
+struct AttnArgs {
+  const void* q;
+  const void* k_live;
+  const void* v_live;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* seed_idx;  // may be null when max_seeds == 0
+  const int32_t* n_seed;    // may be null when max_seeds == 0
+  void* out;
+  float* lse;               // may be null
+  int32_t B, Hq, Hkv, L, d, max_seeds;
+  float scale;              // > 0
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
+struct SelectArgs {
+  const float* logp;
+  const float* d_in;
+  const float* d_out;
+  const uint8_t* flags;
+  int32_t* seed_idx;
+  int32_t* n_seed;
+  double* score;  // may be null
+  int32_t B, Lr, max_seeds, pos_offset;
+};
+
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+
+}  // namespace cover

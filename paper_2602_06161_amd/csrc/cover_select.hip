@@ -1,0 +1,197 @@
+// COVER stability-aware seed selection with an adaptive revision rate on gfx950
+// (arXiv 2602.06161, Sec. 5.3).
+//
+// One workgroup per batch row.  Per region position j (flags bit 0 = unmasked, bit 1 =
+// excluded):
+//   score s_j  = (-logp_j) (1 + d_in_j) / (1 + d_out_j)       in IEEE fp64, this association
+//   mean       = canonical stride-halving tree sum over U_t (region zero-padded to a power of
+//                two) divided by |U_t|
+//   budget k   = least k with k*k >= #{j in U_t : s_j > mean}  (= ceil(sqrt(n_t pi_t)))
+//   seeds      = the k best eligible positions by (score desc, position asc), emitted ascending
+// Every floating-point step is a single IEEE operation in a fixed order (no contraction, see
+// the pragma below), so the result is bit-identical to any other implementation that follows
+// the same order -- which is what makes the selection reproducible across devices.
+//
+// Scores live in registers (up to 16 per thread); the tree sum runs in LDS; the top-k is k
+// rounds of a wavefront argmax (DPP/bpermute shuffles) plus one cross-wave step.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace cover {
+namespace {
+
+constexpr int kMaxThreads = 1024;
+constexpr int kMaxPer = COVER_MAX_LR / kMaxThreads;  // register-resident scores per thread
+constexpr int kMaxWinners = 128;                     // ceil(sqrt(COVER_MAX_LR))
+static_assert(kMaxWinners * kMaxWinners >= COVER_MAX_LR, "winner list too small");
+
+struct SelParams {
+  const float* logp;
+  const float* d_in;
+  const float* d_out;
+  const uint8_t* flags;
+  int32_t* seed_idx;
+  int32_t* n_seed;
+  double* score;
+  int Lr, P, per, max_seeds, pos_offset;
+};
+
+// (score desc, position asc); position < 0 marks "no candidate"
+__device__ __forceinline__ bool better(double sa, int ja, double sb, int jb) {
+  if (ja < 0) return false;
+  if (jb < 0) return true;
+  return sa > sb || (sa == sb && ja < jb);
+}
+
+__device__ __forceinline__ int ceil_isqrt(int c) {
+  int r = (int)sqrt((double)c);
+  while (r * r < c) ++r;
+  while (r > 0 && (r - 1) * (r - 1) >= c) --r;
+  return r;
+}
+
+__global__ __launch_bounds__(kMaxThreads) void cover_select_kernel(const SelParams p) {
+  extern __shared__ double tree[];  // P doubles
+  __shared__ int cnt[3];
+  __shared__ double red_s[kMaxThreads / 64];
+  __shared__ int red_j[kMaxThreads / 64];
+  __shared__ int winners[kMaxWinners];
+  __shared__ int win_now;
+
+  const int b = blockIdx.x, tid = threadIdx.x, nth = blockDim.x;
+  const int lane = tid & 63, wv = tid >> 6, nwv = nth >> 6;
+  const int64_t base = (int64_t)b * p.Lr;
+  if (tid < 3) cnt[tid] = 0;
+  __syncthreads();
+
+  // scores (positions tid + m * nth)
+  double sc[kMaxPer];
+  uint32_t emask = 0, umask = 0;
+  int nu = 0, ne = 0;
+#pragma unroll
+  for (int m = 0; m < kMaxPer; ++m) {
+    sc[m] = 0.0;
+    if (m < p.per) {
+      const int j = tid + m * nth;
+      if (j < p.Lr) {
+        const uint8_t f = p.flags[base + j];
+        if (f & 1u) {
+          const double u = -(double)p.logp[base + j];
+          const double num = u * (1.0 + (double)p.d_in[base + j]);
+          sc[m] = num / (1.0 + (double)p.d_out[base + j]);
+          umask |= 1u << m;
+          ++nu;
+          if (!(f & 2u)) {
+            emask |= 1u << m;
+            ++ne;
+          }
+        }
+        if (p.score) p.score[base + j] = sc[m];
+      }
+      if (j < p.P) tree[j] = sc[m];
+    }
+  }
+  if (nu) atomicAdd(&cnt[0], nu);
+  if (ne) atomicAdd(&cnt[1], ne);
+  __syncthreads();
+
+  // canonical tree: a[i] += a[i + stride] for stride = P/2, P/4, ..., 1
+  for (int stride = p.P >> 1; stride >= 1; stride >>= 1) {
+    for (int i = tid; i < stride; i += nth) tree[i] = tree[i] + tree[i + stride];
+    __syncthreads();
+  }
+  const int n = cnt[0];
+  int c = 0;
+  if (n > 0) {
+    const double mean = tree[0] / (double)n;
+#pragma unroll
+    for (int m = 0; m < kMaxPer; ++m)
+      if (((umask >> m) & 1u) && sc[m] > mean) ++c;
+  }
+  if (c) atomicAdd(&cnt[2], c);
+  __syncthreads();
+  int k = ceil_isqrt(cnt[2]);
+  k = min(k, cnt[1]);
+  k = min(k, p.max_seeds);
+
+  for (int t = 0; t < k; ++t) {
+    double bs = 0.0;
+    int bj = -1;
+#pragma unroll
+    for (int m = 0; m < kMaxPer; ++m) {
+      if ((emask >> m) & 1u) {
+        const int j = tid + m * nth;
+        if (better(sc[m], j, bs, bj)) { bs = sc[m]; bj = j; }
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const double os = __shfl_xor(bs, off);
+      const int oj = __shfl_xor(bj, off);
+      if (better(os, oj, bs, bj)) { bs = os; bj = oj; }
+    }
+    if (lane == 0) { red_s[wv] = bs; red_j[wv] = bj; }
+    __syncthreads();
+    if (tid == 0) {
+      double s0 = red_s[0];
+      int j0 = red_j[0];
+      for (int w = 1; w < nwv; ++w)
+        if (better(red_s[w], red_j[w], s0, j0)) { s0 = red_s[w]; j0 = red_j[w]; }
+      winners[t] = j0;
+      win_now = j0;
+    }
+    __syncthreads();
+    const int w = win_now;
+    if (w >= 0 && w % nth == tid) emask &= ~(1u << (w / nth));
+  }
+  __syncthreads();
+
+  int32_t* out = p.seed_idx + (int64_t)b * p.max_seeds;
+  if (tid < k) {
+    const int w = winners[tid];
+    int rank = 0;
+    for (int u = 0; u < k; ++u) rank += winners[u] < w;
+    out[rank] = w + p.pos_offset;
+  }
+  for (int t = k + tid; t < p.max_seeds; t += nth) out[t] = -1;
+  if (tid == 0) p.n_seed[b] = k;
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
+  SelParams p;
+  p.logp = a.logp;
+  p.d_in = a.d_in;
+  p.d_out = a.d_out;
+  p.flags = a.flags;
+  p.seed_idx = a.seed_idx;
+  p.n_seed = a.n_seed;
+  p.score = a.score;
+  p.Lr = a.Lr;
+  p.max_seeds = a.max_seeds;
+  p.pos_offset = a.pos_offset;
+  int P = 1;
+  while (P < a.Lr) P <<= 1;
+  p.P = P;
+  int nth = P < 64 ? 64 : (P > kMaxThreads ? kMaxThreads : P);
+  p.per = (P + nth - 1) / nth;
+  const size_t lds = (size_t)P * sizeof(double);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void*)cover_select_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       COVER_MAX_LR * (int)sizeof(double));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(cover_select_kernel, dim3((unsigned)a.B), dim3(nth), lds, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

@@ -1,0 +1,115 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every function
+``include/cover.h`` declares, and rejects bad descriptors before enqueuing anything (the
+rejected calls below pass no valid device memory, so reaching a launch would fail)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_06161_amd import cover
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cover.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(cover.LIB), reason="libcover.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(cover_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(cover.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = cover.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version():
+    assert cover.status_str(cover.COVER_OK) == "COVER_OK"
+    assert cover.status_str(cover.COVER_ERR_INVALID) == "COVER_ERR_INVALID"
+    assert cover.status_str(cover.COVER_ERR_UNSUPPORTED) == "COVER_ERR_UNSUPPORTED"
+    assert cover.status_str(cover.COVER_ERR_HIP) == "COVER_ERR_HIP"
+    assert cover.version() == 100
+
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced: every case below fails validation first
+
+
+def _attn(desc, q=FAKE, k=FAKE, out=FAKE, si=FAKE, ns=FAKE, lse=None):
+    lib = cover.lib()
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.cover_attn_fwd(p(q), p(k), p(k), p(k), p(k), p(si), p(ns), p(out), p(lse),
+                              None if desc is None else ctypes.byref(desc), None)
+
+
+def _good(**kw):
+    d = dict(B=1, Hq=4, Hkv=2, L=64, d=128, max_seeds=4, dtype=cover.COVER_BF16, scale=0.0,
+             q_sb=4 * 64 * 128, q_sh=64 * 128, q_sl=128, kv_sb=2 * 64 * 128, kv_sh=64 * 128, kv_sl=128)
+    d.update(kw)
+    return cover.AttnDesc(**d)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(B=-1), cover.COVER_ERR_INVALID),
+    (dict(Hq=0), cover.COVER_ERR_INVALID),
+    (dict(Hkv=3), cover.COVER_ERR_INVALID),            # 4 % 3 != 0
+    (dict(L=-5), cover.COVER_ERR_INVALID),
+    (dict(max_seeds=-1), cover.COVER_ERR_INVALID),
+    (dict(dtype=7), cover.COVER_ERR_INVALID),
+    (dict(scale=-1.0), cover.COVER_ERR_INVALID),
+    (dict(scale=float("nan")), cover.COVER_ERR_INVALID),
+    (dict(d=96), cover.COVER_ERR_UNSUPPORTED),
+    (dict(d=0), cover.COVER_ERR_INVALID),
+    (dict(L=cover.COVER_MAX_L + 1), cover.COVER_ERR_UNSUPPORTED),
+    (dict(q_sl=100), cover.COVER_ERR_INVALID),          # not a multiple of 8 bf16 elements
+    (dict(kv_sl=64), cover.COVER_ERR_INVALID),          # rows would overlap
+    (dict(q_sh=-8), cover.COVER_ERR_INVALID),
+])
+def test_attn_descriptor_errors(kw, expect):
+    assert _attn(_good(**kw)) == expect
+
+
+def test_attn_pointer_errors():
+    assert _attn(None) == cover.COVER_ERR_INVALID
+    assert _attn(_good(), q=None) == cover.COVER_ERR_INVALID
+    assert _attn(_good(), q=FAKE + 8) == cover.COVER_ERR_INVALID     # misaligned
+    assert _attn(_good(), out=None) == cover.COVER_ERR_INVALID
+    assert _attn(_good(), si=None) == cover.COVER_ERR_INVALID        # max_seeds > 0
+    assert _attn(_good(), ns=FAKE + 2) == cover.COVER_ERR_INVALID
+    assert _attn(_good(), lse=FAKE + 2) == cover.COVER_ERR_INVALID
+
+
+def test_attn_empty_problems_are_no_ops():
+    # nothing to compute: success without touching (invalid) memory
+    assert _attn(_good(B=0), q=None, k=None, out=None) == cover.COVER_OK
+    assert _attn(_good(L=0), q=None, k=None, out=None) == cover.COVER_OK
+
+
+def _sel(desc, lp=FAKE, fl=FAKE, si=FAKE, ns=FAKE, sc=None):
+    lib = cover.lib()
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.cover_select_seeds(p(lp), p(lp), p(lp), p(fl), p(si), p(ns), p(sc),
+                                  None if desc is None else ctypes.byref(desc), None)
+
+
+def test_select_errors():
+    good = dict(B=1, Lr=256, max_seeds=8, pos_offset=768)
+    assert _sel(None) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "B": -1})) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "Lr": -1})) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "max_seeds": -2})) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "Lr": cover.COVER_MAX_LR + 1})) == cover.COVER_ERR_UNSUPPORTED
+    assert _sel(cover.SelectDesc(**good), ns=None) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**good), si=None) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**good), lp=None) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**good), lp=FAKE + 1) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**good), sc=FAKE + 4) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "pos_offset": 0x7fffff00})) == cover.COVER_ERR_INVALID
+    assert _sel(cover.SelectDesc(**{**good, "B": 0}), lp=None, fl=None, si=None, ns=None) == cover.COVER_OK

@@ -1,0 +1,215 @@
+"""GPU parity of cover_attn_fwd (through the C ABI) against the fp64 oracle.
+
+Bar: fp32 max-abs 1e-5; bf16 |gpu - oracle| <= 2e-2 + 1e-2 |oracle| on out and 2e-2 on lse.
+Small shapes are compared on every row (several query/key tiles and a ragged tail); the
+full-size workloads are compared on every seed row of sampled heads plus random rows, in
+the same launch configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from helpers import announce, check_attn, to_dev
+from paper_2602_06161_amd import cover, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(a, scale=None, **kw):
+    q, kl, vl, kc, vc, si, ns = to_dev(a)
+    out, lse = cover.cover_attn_fwd(q, kl, vl, kc, vc, si, ns, scale=scale or 0.0, **kw)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def _oracle(a, scale=None, rows=None, mode="fast"):
+    args = [a[k] for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx", "n_seed")]
+    return oracle.attn(*args, scale=scale or a["scale"], mode=mode, rows=rows)
+
+
+def _custom(seed, B, Hq, Hkv, L, d, n_seeds, dtype="bf16", positions=None, max_seeds=None):
+    cfg = synth.AttnConfig("custom", B, Hq, Hkv, L, d, dtype, 0, L, n_seeds, "independent")
+    a = synth.attn_inputs(cfg, seed=seed, max_seeds=max_seeds)
+    if positions is not None:
+        pos = np.array(sorted(positions), np.int32)
+        si = np.full((B, max(len(pos), max_seeds or 0)), -1, np.int32)
+        si[:, : len(pos)] = pos
+        a["seed_idx"] = torch.from_numpy(si)
+        a["n_seed"] = torch.full((B,), len(pos), dtype=torch.int32)
+    return a
+
+
+def test_tiny_f32_every_row():
+    announce("tiny fp32 B1 H2 L64 d64, 4 seeds")
+    a = synth.attn_inputs("tiny", seed=0)
+    out, lse = _run(a)
+    ref, lref = _oracle(a, mode="literal")
+    check_attn(out, lse, ref, lref, torch.float32, "tiny")
+
+
+@pytest.mark.parametrize("shape", [(2, 4, 2, 150, 128, 7), (1, 3, 1, 97, 64, 30), (1, 1, 1, 1, 128, 1)])
+def test_f32_multi_tile_ragged(shape):
+    B, Hq, Hkv, L, d, n = shape
+    announce(f"fp32 B{B} Hq{Hq} Hkv{Hkv} L{L} d{d} seeds{n}")
+    a = _custom(1, B, Hq, Hkv, L, d, n, dtype="f32")
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.float32, str(shape))
+
+
+BF16_SHAPES = [
+    (1, 2, 2, 64, 128, 4),
+    (2, 4, 2, 300, 128, 12),
+    (1, 4, 4, 200, 64, 20),
+    (1, 2, 1, 129, 128, 40),
+    (2, 3, 3, 45, 64, 5),
+    (1, 1, 1, 1, 128, 1),
+    (1, 7, 1, 520, 128, 33),
+]
+
+
+@pytest.mark.parametrize("shape", BF16_SHAPES, ids=[str(s) for s in BF16_SHAPES])
+def test_bf16_every_row(shape):
+    B, Hq, Hkv, L, d, n = shape
+    announce(f"bf16 B{B} Hq{Hq} Hkv{Hkv} L{L} d{d} seeds{n}")
+    a = _custom(2, B, Hq, Hkv, L, d, n)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, str(shape))
+
+
+def test_bf16_seeds_on_every_diagonal_block():
+    # each wave's diagonal block: workgroup halves x key parities, plus tile edges
+    pos = [0, 5, 31, 32, 63, 64, 100, 127, 128, 150, 191, 192, 255]
+    announce(f"bf16 diagonal blocks L256 seeds {pos}")
+    a = _custom(3, 1, 2, 2, 256, 128, 0, positions=pos)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "diag-blocks")
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_every_position_a_seed(d):
+    announce(f"bf16 all positions seeds L96 d{d}")
+    a = _custom(4, 1, 2, 2, 96, d, 0, positions=range(96))
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "all-seeds")
+
+
+def test_zero_seeds_and_no_seed_arrays():
+    announce("bf16 zero seeds / max_seeds 0")
+    a = _custom(5, 1, 4, 2, 200, 128, 6)
+    a["n_seed"][:] = 0
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "n_seed=0")
+    q, kl, vl, kc, vc, _, _ = to_dev(a)
+    out2, lse2 = cover.cover_attn_fwd(q, kl, vl, kc, vc)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2) and torch.equal(lse, lse2)
+
+
+def test_nonseed_cache_rows_are_never_read():
+    announce("bf16 non-seed cache rows = NaN")
+    a = _custom(6, 2, 4, 2, 256, 128, 10)
+    out, lse = _run(a)
+    b2 = dict(a)
+    kc, vc = a["k_cache"].clone(), a["v_cache"].clone()
+    for b in range(2):
+        non = np.setdiff1d(np.arange(256), a["seed_idx"][b, : a["n_seed"][b]].numpy())
+        kc[b][:, non] = float("nan")
+        vc[b][:, non] = float("inf")
+    b2["k_cache"], b2["v_cache"] = kc, vc
+    out2, lse2 = _run(b2)
+    assert torch.isfinite(out2.float()).all()
+    assert torch.equal(out, out2) and torch.equal(lse, lse2)
+
+
+def test_seed_row_ignores_its_own_cached_kv():
+    announce("bf16 perturb one seed's own cached K/V")
+    a = _custom(7, 1, 2, 2, 256, 128, 9)
+    out, lse = _run(a)
+    i = int(a["seed_idx"][0, 3])
+    b2 = dict(a)
+    kc, vc = a["k_cache"].clone(), a["v_cache"].clone()
+    kc[0, :, i] += 3.0
+    vc[0, :, i] -= 2.0
+    b2["k_cache"], b2["v_cache"] = kc, vc
+    out2, lse2 = _run(b2)
+    assert torch.equal(out[0, :, i], out2[0, :, i]) and torch.equal(lse[0, :, i], lse2[0, :, i])
+    others = [j for j in range(256) if j != i]
+    assert not torch.equal(out[0][:, others], out2[0][:, others])
+
+
+def test_repeat_runs_bitwise_equal():
+    announce("bf16 determinism")
+    a = synth.attn_inputs("llada", seed=1)
+    o1, l1 = _run(a)
+    o2, l2 = _run(a)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_dominant_cached_diagonal():
+    # Cached diagonal keys aligned with their own query: alpha_i -> 1, the regime where the
+    # post-hoc closed form cancels; the in-softmax substitution must still match.
+    announce("bf16 dominant cached diagonal")
+    a = _custom(8, 1, 2, 2, 192, 128, 16)
+    kc = a["k_cache"].float()
+    q = a["q"].float()
+    for i in a["seed_idx"][0, : a["n_seed"][0]].tolist():
+        for h in range(2):
+            qi = q[0, h, i]
+            kc[0, h, i] = 8.0 * qi / qi.norm() * np.sqrt(128)
+    a["k_cache"] = kc.to(torch.bfloat16)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "dominant-diag")
+
+
+def test_peaky_scores_force_rescaling():
+    announce("bf16 scale 1.0 (peaky rows)")
+    a = _custom(9, 1, 2, 1, 384, 128, 12)
+    out, lse = _run(a, scale=1.0)
+    ref, lref = _oracle(a, scale=1.0)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "scale=1")
+
+
+def test_strided_token_major_layout():
+    announce("bf16 [B,L,H,d] strided views")
+    a = _custom(10, 2, 4, 2, 160, 128, 8)
+    q, kl, vl, kc, vc, si, ns = to_dev(a)
+    t = lambda x: x.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)  # same values, token-major
+    qs, kls, vls, kcs, vcs = map(t, (q, kl, vl, kc, vc))
+    assert qs.stride(2) == 4 * 128
+    out, lse = cover.cover_attn_fwd(qs, kls, vls, kcs, vcs, si, ns)
+    torch.cuda.synchronize()
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "strided")
+
+
+def _sample_rows(a, rng, heads_per_batch=None, n_random=256):
+    c = a["cfg"]
+    rows = []
+    for b in range(c.B):
+        heads = range(c.Hq) if heads_per_batch is None else rng.choice(c.Hq, heads_per_batch, replace=False)
+        for h in heads:
+            for i in a["seed_idx"][b, : a["n_seed"][b]].tolist():
+                rows.append((b * c.Hq + h) * c.L + i)
+    rows += rng.integers(0, c.B * c.Hq * c.L, n_random).tolist()
+    return np.unique(np.array(rows, np.int64))
+
+
+@pytest.mark.parametrize("name,hpb", [("llada", None), ("dream", None), ("batched", 4)])
+def test_full_size_config_sampled_rows(name, hpb):
+    announce(f"{name} full size, sampled rows")
+    a = synth.attn_inputs(name, seed=0)
+    out, lse = _run(a)
+    rows = _sample_rows(a, np.random.default_rng(0), hpb)
+    ref, lref = _oracle(a, rows=rows)
+    c = a["cfg"]
+    o = out.reshape(-1, c.d)[torch.from_numpy(rows).cuda()]
+    l = lse.reshape(-1)[torch.from_numpy(rows).cuda()]
+    check_attn(o, l, ref, lref, torch.bfloat16, name)
+    assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
