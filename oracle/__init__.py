@@ -62,11 +62,18 @@ def _load():
         lib.cover_oracle_select.argtypes = [P, P, P, P, I, I, I, I, P, P, P]
         lib.cover_oracle_token_stats.argtypes = [P, P, I64, I64, P, P, P]
         lib.cover_oracle_attn_stats.argtypes = [P, P, P, P, P, I, I, I, I, I, I, D, I, I, P, P, P, P]
+        lib.cover_oracle_threads.argtypes = []
+        lib.cover_oracle_threads.restype = ctypes.c_int
         for f in (lib.cover_oracle_attn, lib.cover_oracle_attn_closed, lib.cover_oracle_select,
                   lib.cover_oracle_token_stats, lib.cover_oracle_attn_stats):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().cover_oracle_threads())
 
 
 def _f64(x) -> np.ndarray:

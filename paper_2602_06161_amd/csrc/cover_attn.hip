@@ -52,7 +52,7 @@ typedef __attribute__((address_space(3))) char lds_t;
 constexpr int kThreads = 256;
 constexpr int kBM = 128;             // queries per workgroup
 constexpr int kStageKeys = 64;       // keys per pipeline stage = two 32-key wave tiles
-constexpr float kSlack = 8.0f;       // lazy rescale threshold, log2 units
+constexpr float kSlack = 20.0f;      // rescale only when a row max grows by > 2^20
 constexpr float kInitMax = -1.0e30f; // finite "no key seen yet" reference max
 constexpr float kLn2 = 0.693147180559945309f;
 
@@ -62,16 +62,16 @@ struct Tile {
   static constexpr int KS = D / 16;                 // k-steps of S^T = K Q^T
   static constexpr int DB = D / 32;                 // 32-row blocks of O^T
   static constexpr int ROW = D * 2;                 // bytes per row
-  static constexpr int KBYTES = kStageKeys * ROW;   // K half of a stage
-  static constexpr int STAGE = 2 * KBYTES;          // K + V
-  static constexpr int LOADS = kStageKeys * CH / kThreads;
-  static constexpr int DIAG = 2 * 32 * ROW;         // per wave: live K rows + live V rows
-  static constexpr int OFF_DIAG = 2 * STAGE;
+  static constexpr int SBYTES = kStageKeys * ROW;   // one K or V stage of 64 rows
+  static constexpr int LOADS = kStageKeys * CH / kThreads;  // 16-B chunks per thread per tensor
+  static constexpr int RPP = kThreads / CH;         // rows per load pass
+  static constexpr int OFF_K0 = 0, OFF_K1 = SBYTES, OFF_V0 = 2 * SBYTES, OFF_V1 = 3 * SBYTES;
+  static constexpr int MERGE = (DB * 16 + 2) * 64 * 4;  // per-wave merge slot (after the loop)
+  static constexpr int OFF_DIAG = ((4 * SBYTES > 4 * MERGE ? 4 * SBYTES : 4 * MERGE) + 1023) / 1024 * 1024;
+  static constexpr int DIAG = 32 * ROW;             // per wave: live V rows of its diagonal block
   static constexpr int OFF_BITS = OFF_DIAG + 4 * DIAG;
   static constexpr int BYTES = OFF_BITS + COVER_MAX_L / 8;
-  static constexpr int MERGE = (DB * 16 + 2) * 64 * 4;  // per-wave merge slot (after the loop)
   static_assert(LOADS * kThreads == kStageKeys * CH, "stage must split evenly");
-  static_assert(4 * MERGE <= OFF_BITS, "merge slots must fit below the bitmap");
 };
 
 struct Params {
@@ -89,12 +89,14 @@ struct Params {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
-// LDS swizzles: K rows are read 8 rows per LDS cycle at one chunk column (b128 reads), V
-// rows 4 rows x 2 chunks per cycle (transpose reads); XOR-ing the chunk index with the row
-// spreads both patterns over all banks.
+// LDS swizzles.  K rows are read 16 rows per LDS cycle at one logical chunk (b128 reads), so
+// the chunk index is XOR-ed with the row (D = 128) or with row/2 (D = 64, two rows per
+// 256-byte bank window).  V rows are read by transpose reads, 4 rows x 2 chunks per 16-lane
+// group, spread by XOR-ing with 2*(row%4).
 template <int ROW>
 __device__ __forceinline__ uint32_t k_off(int row, int c) {
-  return row * ROW + ((c ^ (row & 7)) << 4);
+  const int sw = (ROW == 256) ? (row & 15) : ((row >> 1) & 7);
+  return row * ROW + ((c ^ sw) << 4);
 }
 template <int ROW>
 __device__ __forceinline__ uint32_t v_off(int row, int c) {
@@ -131,14 +133,15 @@ __device__ __forceinline__ bf16x8 v_operand(const lds_t* vbase, int row0, int db
 
 __device__ __forceinline__ float swap_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
-  return a > b ? a : b;
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float swap_add(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
-__device__ __forceinline__ float fmax2(float a, float b) { return a > b ? a : b; }
+__device__ __forceinline__ float fmax2(float a, float b) { return __builtin_fmaxf(a, b); }
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 template <int N>
 struct IC {
@@ -155,7 +158,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qh = wave & 1;   // which 64-query half of the workgroup tile
-  const int kp = wave >> 1;  // which key parity (32-key tiles 2*it + kp)
+  const int kp = wave >> 1;  // which key parity (32-key tile kp of every 64-key stage)
   const int hl = lane >> 5, l32 = lane & 31;
 
   // ---- workgroup -> (b, h, query tile); consecutive logical tiles share an XCD --------
@@ -170,52 +173,6 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   const __bf16* qbase = p.q + b * p.q_sb + h * p.q_sh;
   const int64_t kvoff = b * p.kv_sb + g * p.kv_sh;
 
-  // ---- seed bitmap of this sequence ---------------------------------------------------
-  uint32_t* bits = (uint32_t*)(smem_raw + T::OFF_BITS);
-  const int nwords = (L + 31) >> 5;
-  for (int w = tid; w < nwords; w += kThreads) bits[w] = 0u;
-  __syncthreads();
-  int ns = 0;
-  if (p.max_seeds > 0) {
-    ns = p.n_seed[b];
-    ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
-  }
-  for (int t = tid; t < ns; t += kThreads) {
-    const int j = p.seed_idx[(int64_t)b * p.max_seeds + t];
-    if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
-  }
-  __syncthreads();
-  auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
-
-  // ---- stage loader (global -> registers -> LDS) ---------------------------------------
-  u32x4 kst[T::LOADS], vst[T::LOADS];
-  auto load_stage = [&](int it) {
-    const int kb = it * kStageKeys;
-#pragma unroll
-    for (int i = 0; i < T::LOADS; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx / T::CH, c = idx % T::CH;
-      const int key = min(kb + row, L - 1);  // rows past L are masked in the scores
-      const bool sd = is_seed(key);
-      const int64_t off = kvoff + (int64_t)key * p.kv_sl + c * 8;
-      kst[i] = *(const u32x4*)((sd ? p.kc : p.kl) + off);
-      vst[i] = *(const u32x4*)((sd ? p.vc : p.vl) + off);
-    }
-  };
-  auto store_stage = [&](int buf) {
-    lds_t* st = smem + buf * T::STAGE;
-#pragma unroll
-    for (int i = 0; i < T::LOADS; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx / T::CH, c = idx % T::CH;
-      lds_write16(st + k_off<T::ROW>(row, c), kst[i]);
-      lds_write16(st + T::KBYTES + v_off<T::ROW>(row, c), vst[i]);
-    }
-  };
-
-  const int n_it = (L + kStageKeys - 1) / kStageKeys;
-  load_stage(0);
-
   // ---- Q fragments (B operand of S^T = K Q^T): query l32 of block qb, d-chunk 2*ks + hl
   bf16x8 qreg[2][T::KS];
 #pragma unroll
@@ -226,93 +183,175 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     for (int ks = 0; ks < T::KS; ++ks) qreg[qb][ks] = *(const bf16x8*)(qrow + ks * 16);
   }
 
+  // ---- seed bitmap of this sequence ---------------------------------------------------
+  // The seed list is read speculatively (all max_seeds entries) together with its length.
+  uint32_t* bits = (uint32_t*)(smem_raw + T::OFF_BITS);
+  const int nwords = (L + 31) >> 5;
+  const int64_t sbase = (int64_t)b * p.max_seeds;
+  int ns = 0;
+  if (p.max_seeds > 0) ns = p.n_seed[b];
+  const int sj0 = tid < p.max_seeds ? p.seed_idx[sbase + tid] : -1;
+  for (int w = tid; w < nwords; w += kThreads) bits[w] = 0u;
+  __syncthreads();
+  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+  if (tid < ns && (unsigned)sj0 < (unsigned)L) atomicOr(&bits[sj0 >> 5], 1u << (sj0 & 31));
+  for (int t = tid + kThreads; t < ns; t += kThreads) {
+    const int j = p.seed_idx[sbase + t];
+    if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
+  }
+  __syncthreads();
+  auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
+
+  // ---- stage order --------------------------------------------------------------------
+  // The two stages holding this tile's diagonal (2qt, 2qt+1) and a ragged last stage are
+  // "special" and processed last, so all earlier stages run through one branch-free loop.
+  const int n_it = (L + kStageKeys - 1) / kStageKeys;
+  constexpr int kNone = 0x7fffffff;
+  // Does any query of this tile (rows q0 .. q0+127) have a seed?  Same answer in every lane.
+  uint32_t tile_bits = 0;
+#pragma unroll
+  for (int w = 0; w < kBM / 32; ++w) tile_bits |= (q0 / 32 + w < nwords) ? bits[q0 / 32 + w] : 0u;
+  const bool tile_seeded = __builtin_amdgcn_readfirstlane(tile_bits) != 0u;
+  int sp0 = tile_seeded ? 2 * qt : kNone;
+  int sp1 = (tile_seeded && 2 * qt + 1 < n_it) ? 2 * qt + 1 : kNone;
+  int sp2 = (L % kStageKeys != 0 && (n_it - 1 != sp0) && (n_it - 1 != sp1)) ? n_it - 1 : kNone;
+  // sorted: sp0 < sp1 < sp2 whenever present; compact missing entries to the end
+  if (sp0 == kNone) { sp0 = sp1; sp1 = sp2; sp2 = kNone; }
+  if (sp0 == kNone) { sp0 = sp1; sp1 = kNone; }
+  if (sp1 == kNone) { sp1 = sp2; sp2 = kNone; }
+  const int nsp = (sp0 != kNone) + (sp1 != kNone) + (sp2 != kNone);
+  const int n_reg = n_it - nsp;
+  auto seq = [=](int i) -> int {  // i-th stage processed
+    if (i >= n_it) i = n_it - 1;
+    if (i >= n_reg) {
+      const int k = i - n_reg;
+      return k == 0 ? sp0 : (k == 1 ? sp1 : sp2);
+    }
+    int j = i;
+    if (j >= sp0) ++j;
+    if (j >= sp1) ++j;
+    if (j >= sp2) ++j;
+    return j;
+  };
+
+  // ---- stage loader: 64 rows of K or V (global -> registers -> LDS) --------------------
+  // Each row comes from the cache if its position is a seed, else from the live tensor.
+  // Thread tid loads chunk (tid % CH) of rows (tid / CH) + RPP * i.  Rows past the end read
+  // row L-1 (never used unmasked).
+  const int lrow = tid / T::CH, lcol = tid % T::CH;
+  const int64_t lane_off = kvoff + (int64_t)lrow * p.kv_sl + lcol * 8;
+  u32x4 kst[T::LOADS], vst[T::LOADS];
+  auto gload = [&](u32x4* regs, const __bf16* live, const __bf16* cache, int stage) {
+    const int kb = stage * kStageKeys;
+    // seed bits of the stage's 64 rows, then of this thread's rows lrow + RPP * i
+    const uint32_t w0 = __builtin_amdgcn_readfirstlane(bits[kb >> 5]);
+    const uint32_t w1 = (kb >> 5) + 1 < nwords ? __builtin_amdgcn_readfirstlane(bits[(kb >> 5) + 1]) : 0u;
+    const uint64_t mrow = ((((uint64_t)w1) << 32) | w0) >> lrow;
+#pragma unroll
+    for (int i = 0; i < T::LOADS; ++i) {
+      const int key = min(kb + lrow + T::RPP * i, L - 1);
+      const bool sd = (mrow >> (T::RPP * i)) & 1u;  // rows past L: live row L-1, masked later
+      const __bf16* src = sd ? cache : live;
+      regs[i] = *(const u32x4*)(src + lane_off + (int64_t)(key - lrow) * p.kv_sl);
+    }
+  };
+  auto kstore = [&](lds_t* buf) {
+#pragma unroll
+    for (int i = 0; i < T::LOADS; ++i) lds_write16(buf + k_off<T::ROW>(lrow + T::RPP * i, lcol), kst[i]);
+  };
+  auto vstore = [&](lds_t* buf) {
+#pragma unroll
+    for (int i = 0; i < T::LOADS; ++i) lds_write16(buf + v_off<T::ROW>(lrow + T::RPP * i, lcol), vst[i]);
+  };
+  lds_t* const K0 = smem + T::OFF_K0;
+  lds_t* const K1 = smem + T::OFF_K1;
+  lds_t* const V0 = smem + T::OFF_V0;
+  lds_t* const V1 = smem + T::OFF_V1;
+
+  u32x4 kst1[T::LOADS];
+  gload(kst, p.kl, p.kc, seq(0));
+  gload(vst, p.vl, p.vc, seq(0));
+  gload(kst1, p.kl, p.kc, seq(1));
+
   // ---- diagonal set-up ------------------------------------------------------------------
-  // Query block kp of this wave (queries qd0 .. qd0+31) has its diagonal in the 32-key tile
-  // starting at key qd0, which has parity kp, i.e. this wave's tile of iteration itd.
-  // In S^T the diagonal entry of query nq sits in lane half (nq/4)%2, register
-  // (nq/8)*4 + nq%4.
+  // Query block kp of this wave (queries qd0 .. qd0+31) has its diagonal in this wave's
+  // 32-key tile of stage itd = qd0 / 64.  In S^T the diagonal entry of query nq sits in lane
+  // half (nq/4)%2, register (nq/8)*4 + nq%4.
   const int qd0 = q0 + qh * 64 + kp * 32;
   const int itd = qd0 / kStageKeys;
   const bool holds_diag = hl == ((l32 >> 2) & 1);
   const int rd = ((l32 >> 3) << 2) | (l32 & 3);
-  const bool diag_seed = holds_diag && (qd0 + l32) < L && is_seed(qd0 + l32);
-  const bool wave_diag = __builtin_amdgcn_ballot_w64(diag_seed) != 0;
-  lds_t* dg = smem + T::OFF_DIAG + wave * T::DIAG;
-  float s_live = 0.0f;
+  const bool qd_seed = (qd0 + l32) < L && is_seed(qd0 + l32);  // this lane's diagonal query
+  const bool diag_seed = holds_diag && qd_seed;
+  const bool wave_diag = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
+  lds_t* const dg = smem + T::OFF_DIAG + wave * T::DIAG;
+  float s_live = 0.0f;  // raw score q_i . k_live_i of this lane's diagonal query
   if (wave_diag) {
-    // live K and V rows of the block's queries (rows past L repeat row L-1; unused)
+    const int qr = min(qd0 + l32, L - 1);
+    const uint32_t* krow = (const uint32_t*)(p.kl + kvoff + (int64_t)qr * p.kv_sl + hl * 8);
+    float acc = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < T::KS; ++ks) {
+      const u32x4 kv = *(const u32x4*)(krow + ks * 8);
+      const u32x4 qv = __builtin_bit_cast(u32x4, kp ? qreg[1][ks] : qreg[0][ks]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
+        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
+      }
+    }
+    s_live = swap_add(acc);
+    // live V rows of the block's queries, row-major, for the epilogue
 #pragma unroll
     for (int i = 0; i < 32 * T::CH / 64; ++i) {
       const int idx = lane + i * 64;
       const int row = idx / T::CH, c = idx % T::CH;
-      const int qr = min(qd0 + row, L - 1);
-      const int64_t off = kvoff + (int64_t)qr * p.kv_sl + c * 8;
-      lds_write16(dg + k_off<T::ROW>(row, c), *(const u32x4*)(p.kl + off));
-      lds_write16(dg + 32 * T::ROW + v_off<T::ROW>(row, c), *(const u32x4*)(p.vl + off));
+      const int vr = min(qd0 + row, L - 1);
+      lds_write16(dg + row * T::ROW + c * 16, *(const u32x4*)(p.vl + kvoff + (int64_t)vr * p.kv_sl + c * 8));
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // live diagonal scores: the diagonal of (live K rows) Q^T for this block
-    f32x16 sl = {};
-#pragma unroll
-    for (int ks = 0; ks < T::KS; ++ks) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(dg + k_off<T::ROW>(l32, 2 * ks + hl)));
-      sl = mfma(a, kp ? qreg[1][ks] : qreg[0][ks], sl);
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r)
-      if (r == rd) s_live = sl[r];
   }
 
-  store_stage(0);
+  // ---- pipeline prologue: K(seq 0), V(seq 0), K(seq 1) resident; S(seq 0) computed ---------
+  kstore(K0);
+  vstore(V0);
+#pragma unroll
+  for (int j = 0; j < T::LOADS; ++j) kst[j] = kst1[j];
+  kstore(K1);
   __syncthreads();
 
-  float m[2] = {kInitMax, kInitMax};
-  float lsum[2] = {0.0f, 0.0f};
-  f32x16 o[2][T::DB];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int db = 0; db < T::DB; ++db) o[qb][db] = (f32x16){};
-
   const float c2 = p.c2;
-
-  for (int it = 0; it < n_it; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < n_it) load_stage(it + 1);
-    const lds_t* st = smem + buf * T::STAGE;
-    const int kbase = it * kStageKeys + kp * 32;  // first key of this wave's tile
-
-    // S^T = K Q^T for both query blocks; each K operand feeds two MFMAs
-    f32x16 s[2] = {(f32x16){}, (f32x16){}};
+  auto qk = [&](const lds_t* kb, f32x16* s) {
+    s[0] = (f32x16){};
+    s[1] = (f32x16){};
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(st + k_off<T::ROW>(kp * 32 + l32, 2 * ks + hl)));
+      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + k_off<T::ROW>(kp * 32 + l32, 2 * ks + hl)));
       s[0] = mfma(a, qreg[0][ks], s[0]);
       s[1] = mfma(a, qreg[1][ks], s[1]);
     }
-    // keys past the end of the sequence take no weight
-    if (kbase + 32 > L) {
+  };
+  // keys of this wave's tile of `stage` past L, and the seed rows' own (cached) column, get
+  // no weight; the live diagonal term is added in the epilogue
+  auto special_fix = [&](int stage, f32x16* s) {
+    if (stage * kStageKeys + kStageKeys > L) {
+      const int kbase = stage * kStageKeys + kp * 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = kbase + ((r >> 2) << 3) + hl * 4 + (r & 3);
-        if (key >= L) { s[0][r] = -INFINITY; s[1][r] = -INFINITY; }
+        const bool ok = kbase + ((r >> 2) << 3) + hl * 4 + (r & 3) < L;
+        s[0][r] = ok ? s[0][r] : -INFINITY;
+        s[1][r] = ok ? s[1][r] : -INFINITY;
       }
     }
-    const bool dtile = wave_diag && it == itd;
-    if (dtile) {
-      // leave-one-out view: the seed row's own column scores against its live key
+    if (wave_diag && stage == itd) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        if (diag_seed && r == rd) {
-          if (kp) s[1][r] = s_live; else s[0][r] = s_live;
-        }
+        const bool hit = diag_seed && r == rd;
+        s[0][r] = (hit && kp == 0) ? -INFINITY : s[0][r];
+        s[1][r] = (hit && kp == 1) ? -INFINITY : s[1][r];
       }
     }
-
-    // online softmax, lazily rescaled
-    float mt[2];
+  };
+  auto rowmax = [&](const f32x16* s, float* mt) {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       float mx = s[qb][0];
@@ -320,8 +359,83 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       for (int r = 1; r < 16; ++r) mx = fmax2(mx, s[qb][r]);
       mt[qb] = swap_max(mx) * c2;
     }
-    const bool need = (mt[0] > m[0] + kSlack) || (mt[1] > m[1] + kSlack);
-    if (__builtin_amdgcn_ballot_w64(need) != 0) {
+  };
+
+  float m[2], lsum[2] = {0.0f, 0.0f};
+  f32x16 o[2][T::DB];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int db = 0; db < T::DB; ++db) o[qb][db] = (f32x16){};
+
+  f32x16 s_cur[2], s_nxt[2];
+  qk(K0, s_cur);
+  special_fix(seq(0), s_cur);
+  {
+    // the first tile fixes each row's reference max (no accumulator to rescale yet)
+    float mt[2];
+    rowmax(s_cur, mt);
+    m[0] = mt[0] > kInitMax ? mt[0] : kInitMax;
+    m[1] = mt[1] > kInitMax ? mt[1] : kInitMax;
+  }
+  __syncthreads();  // every wave has read K(seq 0) before iteration 0 overwrites its buffer
+
+  // softmax of S(seq i) into bf16 P (row sums accumulated), then O^T += V^T P^T
+  auto softmax_pv = [&](const lds_t* vcur) {
+    bf16x8 pk[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float nm = -m[qb];
+      f32x16 pr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[qb][r], c2, nm));
+      float ls = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ls += pr[r];
+      lsum[qb] += ls;
+      pk[qb][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
+      pk[qb][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int db = 0; db < T::DB; ++db) {
+        const bf16x8 a = v_operand<T::ROW>(vcur, kp * 32 + 16 * kk, db, lane);
+        o[0][db] = mfma(a, pk[0][kk], o[0][db]);
+        o[1][db] = mfma(a, pk[1][kk], o[1][db]);
+      }
+    }
+  };
+
+  // ---- steady state: regular stages, no masking, no diagonal, no rescale ----------------
+  // A row whose max grows by more than 2^kSlack over its reference leaves for the general
+  // loop below, which rescales.
+  int i = 0;
+  for (; i < n_reg; ++i) {
+    float mt[2];
+    rowmax(s_cur, mt);
+    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) || (mt[1] > m[1] + kSlack)) != 0) break;
+    gload(kst, p.kl, p.kc, seq(i + 2));
+    gload(vst, p.vl, p.vc, seq(i + 1));
+    qk((i & 1) ? K0 : K1, s_nxt);
+    softmax_pv((i & 1) ? V1 : V0);
+    kstore((i & 1) ? K1 : K0);        // K(seq i+2) replaces K(seq i)
+    vstore((i & 1) ? V0 : V1);  // V(seq i+1) replaces V(seq i-1)
+    __syncthreads();
+    s_cur[0] = s_nxt[0];
+    s_cur[1] = s_nxt[1];
+  }
+  // ---- general step: special tiles, and regular tiles after a rescale ------------------
+  auto general_step = [&](int i, bool special) {
+    const bool more = i + 1 < n_it;
+    if (more) {
+      gload(kst, p.kl, p.kc, seq(i + 2));
+      gload(vst, p.vl, p.vc, seq(i + 1));
+    }
+    if (special) special_fix(seq(i), s_cur);
+    float mt[2];
+    rowmax(s_cur, mt);
+    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) || (mt[1] > m[1] + kSlack)) != 0) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const float mn = mt[qb] > m[qb] + kSlack ? mt[qb] : m[qb];
@@ -332,60 +446,28 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
         for (int db = 0; db < T::DB; ++db) o[qb][db] *= alpha;
       }
     }
-    bf16x8 pk[2][2];
-    bf16x8 pd[2];  // diagonal-only P of the seed block (dtile only)
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const float nm = -m[qb];
-      f32x16 pr;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, nm));
-      float ls = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) ls += pr[r];
-      lsum[qb] += ls;
-      if (dtile && qb == kp) {
-        f32x16 pdg = {};
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (diag_seed && r == rd) { pdg[r] = pr[r]; pr[r] = 0.0f; }
-        }
-        pd[0] = __builtin_convertvector(__builtin_shufflevector(pdg, pdg, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
-        pd[1] = __builtin_convertvector(__builtin_shufflevector(pdg, pdg, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
-      }
-      pk[qb][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
-      pk[qb][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+    if (more) qk((i & 1) ? K0 : K1, s_nxt);
+    softmax_pv((i & 1) ? V1 : V0);
+    if (more) {
+      kstore((i & 1) ? K1 : K0);
+      vstore((i & 1) ? V0 : V1);
     }
-
-    // O^T += V^T P^T; each V operand feeds two MFMAs
-    const lds_t* vb = st + T::KBYTES;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-      for (int db = 0; db < T::DB; ++db) {
-        const bf16x8 a = v_operand<T::ROW>(vb, kp * 32 + 16 * kk, db, lane);
-        o[0][db] = mfma(a, pk[0][kk], o[0][db]);
-        o[1][db] = mfma(a, pk[1][kk], o[1][db]);
-      }
-    }
-    if (dtile) {
-      // the seed row's diagonal weight multiplies its live value row
-      const lds_t* dv = dg + 32 * T::ROW;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-        for (int db = 0; db < T::DB; ++db) {
-          const bf16x8 a = v_operand<T::ROW>(dv, 16 * kk, db, lane);
-          if (kp) o[1][db] = mfma(a, pd[kk], o[1][db]);
-          else o[0][db] = mfma(a, pd[kk], o[0][db]);
-        }
-      }
-    }
-    if (it + 1 < n_it) store_stage(buf ^ 1);
     __syncthreads();
+    s_cur[0] = s_nxt[0];
+    s_cur[1] = s_nxt[1];
+  };
+  // regular stages left after a rescale (rare)
+  for (; i < n_reg; ++i) general_step(i, false);
+  // the (at most three) special stages, straight-line
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    if (i < n_it) {
+      general_step(i, true);
+      ++i;
+    }
   }
 
-  // ---- merge the two key parities, normalise, store ---------------------------------------
+  // ---- merge the two key parities, add the live diagonal term, normalise, store ---------
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) lsum[qb] = swap_add(lsum[qb]);
   // Wave kp finalises its query block kp; the other block goes to the partner wave (w ^ 2).
@@ -404,11 +486,14 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   __syncthreads();
   auto finish = [&](auto qf_) {
     constexpr int QF = decltype(qf_)::value;
+    // seed rows: the live diagonal term, one more element of the row's softmax
+    const float td = qd_seed ? s_live * c2 : -INFINITY;
     const float ma = m[QF], la = lsum[QF];
     const float mb = theirs[NJ * 64 + lane], lb = theirs[(NJ + 1) * 64 + lane];
-    const float mm = fmax2(ma, mb);
+    const float mm = fmax2(fmax2(ma, mb), td);
     const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
-    const float ltot = la * fa + lb * fb;
+    const float fd = __builtin_amdgcn_exp2f(td - mm);
+    const float ltot = la * fa + lb * fb + fd;
     const float inv = 1.0f / ltot;
     const int qf = qd0 + l32;
     if (qf < L) {
@@ -417,13 +502,24 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       for (int db = 0; db < T::DB; ++db) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
+          const int d0 = db * 32 + g4 * 8 + hl * 4;
           f32x4 v;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int j = db * 16 + g4 * 4 + e;
-            v[e] = (o[QF][db][g4 * 4 + e] * fa + theirs[j * 64 + lane] * fb) * inv;
+            v[e] = o[QF][db][g4 * 4 + e] * fa + theirs[j * 64 + lane] * fb;
           }
-          *(bf16x4*)(orow + db * 32 + g4 * 8 + hl * 4) = __builtin_convertvector(v, bf16x4);
+          if (wave_diag) {
+            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(dg + l32 * T::ROW + d0 * 2);
+            v[0] += fd * bf16_lo(raw[0]);
+            v[1] += fd * bf16_hi(raw[0]);
+            v[2] += fd * bf16_lo(raw[1]);
+            v[3] += fd * bf16_hi(raw[1]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] *= inv;
+          *(bf16x4*)(orow + d0) = __builtin_convertvector(v, bf16x4);
         }
       }
       if (p.lse && hl == 0)
