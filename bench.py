@@ -102,14 +102,12 @@ def main() -> int:
     nns = torch.empty((c.B,), device=dev, dtype=torch.int32)
     score = torch.empty((c.B, a["Lr"]), device=dev, dtype=torch.float64)
 
-    def attn():
-        cover.cover_attn_fwd(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
-                             t["seed_idx"], t["n_seed"], out=out, lse=lse, stream=stream)
-
-    def select():
-        cover.cover_select_seeds(t["logp"], t["d_in"], t["d_out"], t["flags"], max_seeds,
-                                 a["pos_offset"], seed_idx=nsi, n_seed=nns, score=score,
-                                 stream=stream)
+    # arguments marshalled once, so the timed loop is not bound by Python launch overhead
+    attn = cover.PreparedAttn(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
+                              t["seed_idx"], t["n_seed"], out=out, lse=lse, stream=stream)
+    select = cover.PreparedSelect(t["logp"], t["d_in"], t["d_out"], t["flags"], max_seeds,
+                                  a["pos_offset"], seed_idx=nsi, n_seed=nns, score=score,
+                                  stream=stream)
 
     do_attn = args.only in (None, "attn")
     do_sel = args.only in (None, "select")

@@ -141,8 +141,9 @@ typedef struct {
  *            U_t, 0 elsewhere.  The results are bit-exact functions of the inputs.
  * Inputs: logp, d_in, d_out fp32 [B,Lr] row-major (logp = log p_j(y_j) <= 0, the model's
  * log-probability of the token currently at j; d_in, d_out >= 0 are the in/out attention
- * masses); flags uint8 [B,Lr].  Inputs at positions outside U_t are not read.  Device-data
- * contract: values on U_t finite, d_in and d_out >= 0.
+ * masses); flags uint8 [B,Lr].  Values at positions outside U_t are ignored (they may be
+ * anything, including non-finite).  Device-data contract: values on U_t finite, d_in and
+ * d_out >= 0.
  * The output layout matches cover_attn_fwd's seed_idx / n_seed, so the next step's
  * attention can consume it without a host round-trip.
  */

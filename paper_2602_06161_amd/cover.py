@@ -159,3 +159,46 @@ def attn_flops(B: int, Hq: int, L: int, d: int) -> int:
 
 def default_scale(d: int) -> float:
     return 1.0 / math.sqrt(d)
+
+
+class PreparedAttn:
+    """A cover_attn_fwd call with its arguments marshalled once, for tight loops: calling it
+    re-launches the kernel on the same tensors (their contents may change between calls)."""
+
+    def __init__(self, q, k_live, v_live, k_cache, v_cache, seed_idx=None, n_seed=None, out=None,
+                 lse=None, scale: float = 0.0, stream=None):
+        self.out, self.lse = cover_attn_fwd(q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed,
+                                            out=out, lse=lse, scale=scale, stream=stream)
+        self._keep = (q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed, self.out, self.lse)
+        max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+        self._desc = attn_desc(q, k_live, max_seeds, scale)
+        self._args = (_ptr(q), _ptr(k_live), _ptr(v_live), _ptr(k_cache), _ptr(v_cache),
+                      _ptr(seed_idx), _ptr(n_seed), _ptr(self.out), _ptr(self.lse),
+                      ctypes.byref(self._desc), _stream(stream))
+        self._fn = lib().cover_attn_fwd
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != COVER_OK:
+            raise CoverError(st, "cover_attn_fwd")
+
+
+class PreparedSelect:
+    """A cover_select_seeds call with its arguments marshalled once (see PreparedAttn)."""
+
+    def __init__(self, logp, d_in, d_out, flags, max_seeds: int, pos_offset: int = 0,
+                 seed_idx=None, n_seed=None, score=None, want_score: bool = True, stream=None):
+        self.seed_idx, self.n_seed, self.score = cover_select_seeds(
+            logp, d_in, d_out, flags, max_seeds, pos_offset, seed_idx=seed_idx, n_seed=n_seed,
+            score=score, want_score=want_score, stream=stream)
+        self._keep = (logp, d_in, d_out, flags, self.seed_idx, self.n_seed, self.score)
+        self._desc = SelectDesc(logp.shape[0], logp.shape[1], max_seeds, pos_offset)
+        self._args = (_ptr(logp), _ptr(d_in), _ptr(d_out), _ptr(flags), _ptr(self.seed_idx),
+                      _ptr(self.n_seed), _ptr(self.score), ctypes.byref(self._desc),
+                      _stream(stream))
+        self._fn = lib().cover_select_seeds
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != COVER_OK:
+            raise CoverError(st, "cover_select_seeds")

@@ -12,8 +12,8 @@
 // the pragma below), so the result is bit-identical to any other implementation that follows
 // the same order -- which is what makes the selection reproducible across devices.
 //
-// Scores live in registers (up to 16 per thread); the tree sum runs in LDS; the top-k is k
-// rounds of a wavefront argmax (DPP/bpermute shuffles) plus one cross-wave step.
+// Regions of up to 1024 positions run on one wave (scores in registers, DPP reductions, no
+// barriers); larger regions use one workgroup of up to 1024 threads with the tree in LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -162,6 +162,135 @@ __global__ __launch_bounds__(kMaxThreads) void cover_select_kernel(const SelPara
   if (tid == 0) p.n_seed[b] = k;
 }
 
+// ---------------------------------------------------------------------------------------
+// Single-wave variant for regions of up to 1024 positions (the paper's generation lengths
+// are 256 and 512): no barriers and no LDS.  Lane l holds positions l + 64 m.  The tree,
+// the counts and the ordering are the same operations as above, so the results are the
+// same bits.
+// ---------------------------------------------------------------------------------------
+constexpr int kWaveMaxPer = 16;  // 64 lanes x 16 = 1024 positions
+
+// DPP full-wave reductions (result valid in lane 63): quad xor 1 and 2, half-row and row
+// mirrors, then row broadcasts 15 and 31.
+template <class F>
+__device__ __forceinline__ int wave_reduce_i32(int x, F op) {
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));  // row_bcast:15
+  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));  // row_bcast:31
+  return x;
+}
+template <int CTRL, int RMASK>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)u, (int)(uint32_t)u, CTRL, RMASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(u >> 32), (int)(uint32_t)(u >> 32), CTRL, RMASK, 0xF, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+// max over the wave of fp64 values (no NaN): result in lane 63
+__device__ __forceinline__ double wave_max_f64(double x) {
+  x = fmax(x, dpp_f64<0xB1, 0xF>(x));
+  x = fmax(x, dpp_f64<0x4E, 0xF>(x));
+  x = fmax(x, dpp_f64<0x141, 0xF>(x));
+  x = fmax(x, dpp_f64<0x140, 0xF>(x));
+  x = fmax(x, dpp_f64<0x142, 0xA>(x));
+  x = fmax(x, dpp_f64<0x143, 0xC>(x));
+  return x;
+}
+__device__ __forceinline__ double lane63_f64(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+__global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int64_t base = (int64_t)b * p.Lr;
+  const int E = p.per;  // positions per lane (P / 64, at least 1)
+  double sc[kWaveMaxPer];
+  uint32_t umask = 0, emask = 0;
+#pragma unroll
+  for (int m = 0; m < kWaveMaxPer; ++m) {
+    sc[m] = 0.0;
+    const int j = lane + 64 * m;
+    if (m < E && j < p.Lr) {
+      const uint8_t f = p.flags[base + j];
+      const float lp = p.logp[base + j], di = p.d_in[base + j], dq = p.d_out[base + j];
+      if (f & 1u) {
+        const double u = -(double)lp;
+        const double num = u * (1.0 + (double)di);
+        sc[m] = num / (1.0 + (double)dq);
+        umask |= 1u << m;
+        if (!(f & 2u)) emask |= 1u << m;
+      }
+      if (p.score) p.score[base + j] = sc[m];
+    }
+  }
+  int n = 0, n_elig = 0;
+#pragma unroll
+  for (int m = 0; m < kWaveMaxPer; ++m) {
+    n += __builtin_popcountll(__builtin_amdgcn_ballot_w64((umask >> m) & 1u));
+    n_elig += __builtin_popcountll(__builtin_amdgcn_ballot_w64((emask >> m) & 1u));
+  }
+  // canonical tree over P = 64 E (or P < 64) positions: strides >= 64 stay in-lane
+  double a[kWaveMaxPer];
+#pragma unroll
+  for (int m = 0; m < kWaveMaxPer; ++m) a[m] = sc[m];
+#pragma unroll
+  for (int half = kWaveMaxPer / 2; half >= 1; half >>= 1)
+    if (half < E)
+#pragma unroll
+      for (int m = 0; m < half; ++m) a[m] = a[m] + a[m + half];
+  double acc = a[0];
+  for (int stride = (p.P < 64 ? p.P : 64) >> 1; stride >= 1; stride >>= 1) {
+    const double o = __shfl_down(acc, stride);
+    acc = acc + o;  // lanes >= stride compute values that are never used
+  }
+  const uint64_t tb = __builtin_bit_cast(uint64_t, acc);
+  const double total = __builtin_bit_cast(double, ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(tb >> 32)) << 32) |
+                                                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)tb));
+  int c = 0;
+  if (n > 0) {
+    const double mean = total / (double)n;
+#pragma unroll
+    for (int m = 0; m < kWaveMaxPer; ++m)
+      c += __builtin_popcountll(__builtin_amdgcn_ballot_w64(((umask >> m) & 1u) && sc[m] > mean));
+  }
+  int k = ceil_isqrt(c);
+  k = min(k, n_elig);
+  k = min(k, p.max_seeds);
+
+  int mine = 0x7fffffff;  // lane t keeps the t-th winner
+  for (int t = 0; t < k; ++t) {
+    double bs = -1.0;
+    int bj = -1;
+#pragma unroll
+    for (int m = 0; m < kWaveMaxPer; ++m) {
+      if ((emask >> m) & 1u) {
+        const int j = lane + 64 * m;
+        if (better(sc[m], j, bs, bj)) { bs = sc[m]; bj = j; }
+      }
+    }
+    // best score over the wave, then the smallest position holding it
+    const double gmax = lane63_f64(wave_max_f64(bj >= 0 ? bs : -INFINITY));
+    const int cand = (bj >= 0 && bs == gmax) ? bj : 0x7fffffff;
+    const int w = __builtin_amdgcn_readlane(wave_reduce_i32(cand, [](int x, int y) { return x < y ? x : y; }), 63);
+    if ((w & 63) == lane) emask &= ~(1u << (w >> 6));
+    if (lane == t) mine = w;
+  }
+  int32_t* out = p.seed_idx + (int64_t)b * p.max_seeds;
+  if (lane < k) {
+    int rank = 0;
+    for (int u = 0; u < k; ++u) rank += __builtin_amdgcn_readlane(mine, u) < mine;
+    out[rank] = mine + p.pos_offset;
+  }
+  for (int t = k + lane; t < p.max_seeds; t += 64) out[t] = -1;
+  if (lane == 0) p.n_seed[b] = k;
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
@@ -179,6 +308,11 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   int P = 1;
   while (P < a.Lr) P <<= 1;
   p.P = P;
+  if (P <= 64 * kWaveMaxPer) {
+    p.per = P > 64 ? P / 64 : 1;
+    hipLaunchKernelGGL(cover_select_wave_kernel, dim3((unsigned)a.B), dim3(64), 0, stream, p);
+    return hipGetLastError();
+  }
   int nth = P < 64 ? 64 : (P > kMaxThreads ? kMaxThreads : P);
   p.per = (P + nth - 1) / nth;
   const size_t lds = (size_t)P * sizeof(double);
