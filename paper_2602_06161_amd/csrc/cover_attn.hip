@@ -48,6 +48,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) char lds_t;
+typedef __attribute__((address_space(1))) const char gmem_t;  // global memory, read-only here
 
 constexpr int kThreads = 256;
 constexpr int kBM = 128;             // queries per workgroup
@@ -56,6 +57,10 @@ constexpr float kSlack = 20.0f;      // rescale only when a row max grows by > 2
 constexpr float kInitMax = -1.0e30f; // finite "no key seen yet" reference max
 constexpr float kLn2 = 0.693147180559945309f;
 
+// s_waitcnt immediates waiting for vmcnt <= n only, or for lgkmcnt <= n only
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xf00; }
+constexpr int lgkmcnt_imm(int n) { return 0xf | (3 << 14) | 0x70 | ((n & 15) << 8); }
+
 template <int D>
 struct Tile {
   static constexpr int CH = D / 8;                  // 16-byte chunks per bf16 row
@@ -63,15 +68,12 @@ struct Tile {
   static constexpr int DB = D / 32;                 // 32-row blocks of O^T
   static constexpr int ROW = D * 2;                 // bytes per row
   static constexpr int SBYTES = kStageKeys * ROW;   // one K or V stage of 64 rows
-  static constexpr int LOADS = kStageKeys * CH / kThreads;  // 16-B chunks per thread per tensor
-  static constexpr int RPP = kThreads / CH;         // rows per load pass
-  static constexpr int OFF_K0 = 0, OFF_K1 = SBYTES, OFF_V0 = 2 * SBYTES, OFF_V1 = 3 * SBYTES;
-  static constexpr int MERGE = (DB * 16 + 2) * 64 * 4;  // per-wave merge slot (after the loop)
-  static constexpr int OFF_DIAG = ((4 * SBYTES > 4 * MERGE ? 4 * SBYTES : 4 * MERGE) + 1023) / 1024 * 1024;
-  static constexpr int DIAG = 32 * ROW;             // per wave: live V rows of its diagonal block
-  static constexpr int OFF_BITS = OFF_DIAG + 4 * DIAG;
-  static constexpr int BYTES = OFF_BITS + COVER_MAX_L / 8;
-  static_assert(LOADS * kThreads == kStageKeys * CH, "stage must split evenly");
+  static constexpr int RPI = 1024 / ROW;            // rows per 1-KiB direct-to-LDS wave load
+  static constexpr int IPW = SBYTES / 1024 / 4;     // such loads per wave per stage
+  static constexpr int NJ = DB * 16;                // O^T values per lane per query block
+  // s_waitcnt immediate: at most 2*IPW vector-memory loads outstanding
+  static constexpr int kWaitPrev = vmcnt_imm(2 * IPW);
+  static_assert(NJ * 64 * 4 <= SBYTES, "a wave's merge slot must fit one stage buffer");
 };
 
 struct Params {
@@ -94,18 +96,21 @@ struct Params {
 // 256-byte bank window).  V rows are read by transpose reads, 4 rows x 2 chunks per 16-lane
 // group, spread by XOR-ing with 2*(row%4).
 template <int ROW>
-__device__ __forceinline__ uint32_t k_off(int row, int c) {
-  const int sw = (ROW == 256) ? (row & 15) : ((row >> 1) & 7);
-  return row * ROW + ((c ^ sw) << 4);
+__device__ __forceinline__ int k_swz(int row) {
+  return (ROW == 256) ? (row & 15) : ((row >> 1) & 7);
 }
 template <int ROW>
-__device__ __forceinline__ uint32_t v_off(int row, int c) {
-  return row * ROW + ((c ^ ((row & 3) << 1)) << 4);
+__device__ __forceinline__ int v_swz(int row) {
+  return (row & 3) << 1;
+}
+template <int ROW>
+__device__ __forceinline__ uint32_t k_off(int row, int c) {
+  return row * ROW + ((c ^ k_swz<ROW>(row)) << 4);
 }
 // byte address of element `col` of V row `row`
 template <int ROW>
 __device__ __forceinline__ uint32_t v_elem(int row, int col) {
-  return v_off<ROW>(row, col >> 3) + ((col & 7) << 1);
+  return row * ROW + (((col >> 3) ^ v_swz<ROW>(row)) << 4) + ((col & 7) << 1);
 }
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -113,22 +118,10 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 }
 
 __device__ __forceinline__ u32x4 lds_read16(const lds_t* p) { return *(const __attribute__((address_space(3))) u32x4*)p; }
-__device__ __forceinline__ void lds_write16(lds_t* p, u32x4 v) { *(__attribute__((address_space(3))) u32x4*)p = v; }
 
-// A operand of O^T += V^T P^T for 16 keys starting at stage row `row0`, d-block `db`:
-// lane (G = lane/16, i = lane%16) receives V[row0 + 4*(G/2) + {0..3, 8..11}][db*32 + 16*(G%2) + i].
-template <int ROW>
-__device__ __forceinline__ bf16x8 v_operand(const lds_t* vbase, int row0, int db, int lane) {
-  const int G = lane >> 4, i = lane & 15;
-  const int row = row0 + 4 * (G >> 1) + (i >> 2);
-  const int col = db * 32 + 16 * (G & 1) + 4 * (i & 3);
-  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) i16x4*)(vbase + v_elem<ROW>(row, col)));
-  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) i16x4*)(vbase + v_elem<ROW>(row + 8, col)));
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
-  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return __builtin_bit_cast(bf16x8, v);
+// Half of the A operand of O^T += V^T P^T: transpose read of 4 V rows x 4 columns per lane.
+__device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
 }
 
 __device__ __forceinline__ float swap_max(float x) {
@@ -140,6 +133,7 @@ __device__ __forceinline__ float swap_add(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 __device__ __forceinline__ float fmax2(float a, float b) { return __builtin_fmaxf(a, b); }
+__device__ __forceinline__ float fmax3(float a, float b, float c) { return __builtin_fmaxf(__builtin_fmaxf(a, b), c); }
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -148,11 +142,57 @@ struct IC {
   static constexpr int value = N;
 };
 
+// 16-byte direct global -> LDS load: lane l's bytes land at dst + 16 l.
+__device__ __forceinline__ void dma16(const void* src, lds_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+
+// Instruction order of one branch-free pipeline step (one wave issues in order, so the
+// matrix core stays busy only if vector work is threaded between the MFMAs): K operand
+// reads, a few exponentials to cover their latency, the S = K Q^T MFMAs each followed by
+// softmax work, the V operand reads, then the PV MFMAs each followed by the remaining
+// vector work (next tile's copies and range check, row sums).
+template <class T>
+__device__ __forceinline__ void step_schedule() {
+  constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
+  constexpr int nqk = 2 * T::KS, npv = 4 * T::DB;
+  __builtin_amdgcn_sched_group_barrier(kDsRead, T::KS, 0);
+  __builtin_amdgcn_sched_group_barrier(kValu, 6, 0);
+#pragma unroll
+  for (int k = 0; k < nqk / 2; ++k) {
+    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * 2 * T::DB, 0);
+#pragma unroll
+  for (int k = 0; k < nqk / 2; ++k) {
+    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
+  }
+#pragma unroll
+  for (int k = 0; k < npv; ++k) {
+    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kValu, 4, 0);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Params p) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(16))) char smem_raw[T::BYTES];
-  lds_t* smem = (lds_t*)smem_raw;
+  // Two K and two V stage buffers; the loads for a stage are staged in registers one step
+  // ahead.
+  __shared__ __attribute__((aligned(1024))) char sK0[T::SBYTES];
+  __shared__ __attribute__((aligned(1024))) char sK1[T::SBYTES];
+  __shared__ __attribute__((aligned(1024))) char sV0[T::SBYTES];
+  __shared__ __attribute__((aligned(1024))) char sV1[T::SBYTES];
+  __shared__ __attribute__((aligned(1024))) char sDiag0[32 * T::ROW];
+  __shared__ __attribute__((aligned(1024))) char sDiag1[32 * T::ROW];
+  __shared__ __attribute__((aligned(1024))) char sDiag2[32 * T::ROW];
+  __shared__ __attribute__((aligned(1024))) char sDiag3[32 * T::ROW];
+  __shared__ __attribute__((aligned(16))) float sML[4 * 2 * 64];
+  __shared__ uint32_t bits[COVER_MAX_L / 32];
+  auto kbuf = [&](int n) -> lds_t* { return (lds_t*)(n == 0 ? sK0 : sK1); };
+  auto vbuf = [&](int n) -> lds_t* { return (lds_t*)(n == 0 ? sV0 : sV1); };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -174,6 +214,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   const int64_t kvoff = b * p.kv_sb + g * p.kv_sh;
 
   // ---- Q fragments (B operand of S^T = K Q^T): query l32 of block qb, d-chunk 2*ks + hl
+  const float c2 = p.c2;
   bf16x8 qreg[2][T::KS];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
@@ -185,13 +226,13 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
 
   // ---- seed bitmap of this sequence ---------------------------------------------------
   // The seed list is read speculatively (all max_seeds entries) together with its length.
-  uint32_t* bits = (uint32_t*)(smem_raw + T::OFF_BITS);
   const int nwords = (L + 31) >> 5;
   const int64_t sbase = (int64_t)b * p.max_seeds;
   int ns = 0;
   if (p.max_seeds > 0) ns = p.n_seed[b];
   const int sj0 = tid < p.max_seeds ? p.seed_idx[sbase + tid] : -1;
-  for (int w = tid; w < nwords; w += kThreads) bits[w] = 0u;
+  // words past the sequence are cleared too: per-stage lookups read two words per stage
+  for (int w = tid; w < 2 * ((L + kStageKeys - 1) / kStageKeys); w += kThreads) bits[w] = 0u;
   __syncthreads();
   ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
   if (tid < ns && (unsigned)sj0 < (unsigned)L) atomicOr(&bits[sj0 >> 5], 1u << (sj0 & 31));
@@ -202,76 +243,108 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   __syncthreads();
   auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
 
-  // ---- stage order --------------------------------------------------------------------
-  // The two stages holding this tile's diagonal (2qt, 2qt+1) and a ragged last stage are
-  // "special" and processed last, so all earlier stages run through one branch-free loop.
+  // ---- stage order ---------------------------------------------------------------------
+  // Stages of 64 keys.  Up to three need per-element care -- the two holding this tile's
+  // diagonal when the tile has seeds, and a ragged last stage -- and are processed last, so
+  // every earlier stage runs through one branch-free step.
   const int n_it = (L + kStageKeys - 1) / kStageKeys;
   constexpr int kNone = 0x7fffffff;
-  // Does any query of this tile (rows q0 .. q0+127) have a seed?  Same answer in every lane.
   uint32_t tile_bits = 0;
 #pragma unroll
   for (int w = 0; w < kBM / 32; ++w) tile_bits |= (q0 / 32 + w < nwords) ? bits[q0 / 32 + w] : 0u;
   const bool tile_seeded = __builtin_amdgcn_readfirstlane(tile_bits) != 0u;
+  const int spC = __builtin_amdgcn_readfirstlane(L % kStageKeys != 0 ? n_it - 1 : -1);  // ragged
+  // the special stages in increasing order (kNone when absent)
   int sp0 = tile_seeded ? 2 * qt : kNone;
   int sp1 = (tile_seeded && 2 * qt + 1 < n_it) ? 2 * qt + 1 : kNone;
-  int sp2 = (L % kStageKeys != 0 && (n_it - 1 != sp0) && (n_it - 1 != sp1)) ? n_it - 1 : kNone;
-  // sorted: sp0 < sp1 < sp2 whenever present; compact missing entries to the end
+  int sp2 = (spC >= 0 && spC != sp0 && spC != sp1) ? spC : kNone;
   if (sp0 == kNone) { sp0 = sp1; sp1 = sp2; sp2 = kNone; }
   if (sp0 == kNone) { sp0 = sp1; sp1 = kNone; }
   if (sp1 == kNone) { sp1 = sp2; sp2 = kNone; }
-  const int nsp = (sp0 != kNone) + (sp1 != kNone) + (sp2 != kNone);
-  const int n_reg = n_it - nsp;
-  auto seq = [=](int i) -> int {  // i-th stage processed
+  sp0 = __builtin_amdgcn_readfirstlane(sp0);
+  sp1 = __builtin_amdgcn_readfirstlane(sp1);
+  sp2 = __builtin_amdgcn_readfirstlane(sp2);
+  const int n_reg = n_it - (sp0 != kNone) - (sp1 != kNone) - (sp2 != kNone);
+  // stage processed at position i (positions past the end repeat the last one)
+  auto seq = [=](int i) -> int {
     if (i >= n_it) i = n_it - 1;
     if (i >= n_reg) {
       const int k = i - n_reg;
       return k == 0 ? sp0 : (k == 1 ? sp1 : sp2);
     }
+    // regular position i skips the special stages: j >= s  <=>  s - 1 - j < 0
     int j = i;
-    if (j >= sp0) ++j;
-    if (j >= sp1) ++j;
-    if (j >= sp2) ++j;
-    return j;
+    j += (int)((uint32_t)(sp0 - 1 - j) >> 31);
+    j += (int)((uint32_t)(sp1 - 1 - j) >> 31);
+    j += (int)((uint32_t)(sp2 - 1 - j) >> 31);
+    return __builtin_amdgcn_readfirstlane(j);
+  };
+  // stages 0..63 holding a seed, one bit each (later stages consult the bitmap)
+  const uint64_t dirty64 = __builtin_amdgcn_ballot_w64(
+      2 * lane < nwords && (bits[2 * lane] | (2 * lane + 1 < nwords ? bits[2 * lane + 1] : 0u)) != 0u);
+  auto dirty = [&](int stage) -> bool {
+    if (stage < 64) return (dirty64 >> stage) & 1u;
+    const uint32_t w0 = __builtin_amdgcn_readfirstlane(bits[2 * stage]);
+    const uint32_t w1 = __builtin_amdgcn_readfirstlane(bits[2 * stage + 1]);
+    return (w0 | w1) != 0u;
   };
 
-  // ---- stage loader: 64 rows of K or V (global -> registers -> LDS) --------------------
-  // Each row comes from the cache if its position is a seed, else from the live tensor.
-  // Thread tid loads chunk (tid % CH) of rows (tid / CH) + RPP * i.  Rows past the end read
-  // row L-1 (never used unmasked).
-  const int lrow = tid / T::CH, lcol = tid % T::CH;
-  const int64_t lane_off = kvoff + (int64_t)lrow * p.kv_sl + lcol * 8;
-  u32x4 kst[T::LOADS], vst[T::LOADS];
-  auto gload = [&](u32x4* regs, const __bf16* live, const __bf16* cache, int stage) {
-    const int kb = stage * kStageKeys;
-    // seed bits of the stage's 64 rows, then of this thread's rows lrow + RPP * i
-    const uint32_t w0 = __builtin_amdgcn_readfirstlane(bits[kb >> 5]);
-    const uint32_t w1 = (kb >> 5) + 1 < nwords ? __builtin_amdgcn_readfirstlane(bits[(kb >> 5) + 1]) : 0u;
-    const uint64_t mrow = ((((uint64_t)w1) << 32) | w0) >> lrow;
+  // ---- stage loads -------------------------------------------------------------------------
+  // A stage is 64 rows; each wave moves IPW KiB of it, 16 bytes per lane per KiB, through
+  // registers: load j of this wave holds row (wave*IPW + j)*RPI + lane/CH, physical chunk
+  // lane%CH, which is the row's logical chunk (physical ^ swizzle), and is stored to LDS at
+  // (wave*IPW + j)*1024 + 16*lane.  A row comes from the cache when its position is a seed;
+  // rows past L (ragged last stage) repeat row L-1 (their scores are masked).
+  auto ld_row = [&](int j) { return (wave * T::IPW + j) * T::RPI + lane / T::CH; };
+  auto ld_chunk = [&](int j, bool is_v) -> uint32_t {
+    const int row = ld_row(j), pc = lane % T::CH;
+    return (uint32_t)((pc ^ (is_v ? (v_swz<T::ROW>(row) & (T::CH - 1)) : k_swz<T::ROW>(row))) << 4);
+  };
+  const int64_t row_bytes = p.kv_sl * 2;
+  const int64_t stage_bytes = kStageKeys * row_bytes;
+  uint32_t offK[T::IPW], offV[T::IPW];
 #pragma unroll
-    for (int i = 0; i < T::LOADS; ++i) {
-      const int key = min(kb + lrow + T::RPP * i, L - 1);
-      const bool sd = (mrow >> (T::RPP * i)) & 1u;  // rows past L: live row L-1, masked later
-      const __bf16* src = sd ? cache : live;
-      regs[i] = *(const u32x4*)(src + lane_off + (int64_t)(key - lrow) * p.kv_sl);
+  for (int j = 0; j < T::IPW; ++j) {
+    offK[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, false);
+    offV[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, true);
+  }
+  auto uniform_ptr = [](const void* ptr) -> gmem_t* {
+    const uint64_t v = (uint64_t)ptr;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (gmem_t*)(((uint64_t)hi << 32) | lo);
+  };
+  gmem_t* const klb = uniform_ptr(p.kl + kvoff);
+  gmem_t* const kcb = uniform_ptr(p.kc + kvoff);
+  gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
+  gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
+  // Issue the loads of one stage (64 rows) of K or V into st[0..IPW).  Stages without seeds
+  // and within L use a scalar base and per-lane 32-bit offsets; the others choose each row's
+  // source and clamp rows past L.
+  typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+  auto ld = [&](u32x4* st, gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v,
+                int stage_in) {
+    const int stage = __builtin_amdgcn_readfirstlane(stage_in);
+    const int kb = stage * kStageKeys;
+    if (stage != spC && !dirty(stage)) {
+      gmem_t* lb = uniform_ptr((const void*)(live + stage * stage_bytes));
+#pragma unroll
+      for (int j = 0; j < T::IPW; ++j) st[j] = *(gu32x4*)(lb + off[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < T::IPW; ++j) {
+        const int key = min(kb + ld_row(j), L - 1);
+        gmem_t* src = is_seed(key) ? cache : live;
+        st[j] = *(gu32x4*)(src + key * row_bytes + ld_chunk(j, is_v));
+      }
     }
   };
-  auto kstore = [&](lds_t* buf) {
+  lds_t* const lds_slot = (lds_t*)nullptr + wave * (T::IPW * 1024) + lane * 16;  // within a buffer
+  auto st = [&](const u32x4* stg, lds_t* buf) {
 #pragma unroll
-    for (int i = 0; i < T::LOADS; ++i) lds_write16(buf + k_off<T::ROW>(lrow + T::RPP * i, lcol), kst[i]);
+    for (int j = 0; j < T::IPW; ++j)
+      *(__attribute__((address_space(3))) u32x4*)(buf + (uintptr_t)lds_slot + j * 1024) = stg[j];
   };
-  auto vstore = [&](lds_t* buf) {
-#pragma unroll
-    for (int i = 0; i < T::LOADS; ++i) lds_write16(buf + v_off<T::ROW>(lrow + T::RPP * i, lcol), vst[i]);
-  };
-  lds_t* const K0 = smem + T::OFF_K0;
-  lds_t* const K1 = smem + T::OFF_K1;
-  lds_t* const V0 = smem + T::OFF_V0;
-  lds_t* const V1 = smem + T::OFF_V1;
-
-  u32x4 kst1[T::LOADS];
-  gload(kst, p.kl, p.kc, seq(0));
-  gload(vst, p.vl, p.vc, seq(0));
-  gload(kst1, p.kl, p.kc, seq(1));
 
   // ---- diagonal set-up ------------------------------------------------------------------
   // Query block kp of this wave (queries qd0 .. qd0+31) has its diagonal in this wave's
@@ -284,8 +357,25 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   const bool qd_seed = (qd0 + l32) < L && is_seed(qd0 + l32);  // this lane's diagonal query
   const bool diag_seed = holds_diag && qd_seed;
   const bool wave_diag = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
-  lds_t* const dg = smem + T::OFF_DIAG + wave * T::DIAG;
-  float s_live = 0.0f;  // raw score q_i . k_live_i of this lane's diagonal query
+
+  // Seed rows need the live value row of their own position in the epilogue: the 32 rows
+  // of this wave's diagonal block go to its sDiag slot (K swizzle).
+  lds_t* const dg = (lds_t*)(wave == 0 ? sDiag0 : (wave == 1 ? sDiag1 : (wave == 2 ? sDiag2 : sDiag3)));
+  if (wave_diag) {
+    u32x4 dv[32 * T::ROW / 1024];
+#pragma unroll
+    for (int j = 0; j < 32 * T::ROW / 1024; ++j) {
+      const int row = j * T::RPI + lane / T::CH, pc = lane % T::CH;
+      const int vr = min(qd0 + row, L - 1);
+      dv[j] = *(gu32x4*)(vlb + vr * row_bytes + ((pc ^ k_swz<T::ROW>(row)) << 4));
+    }
+#pragma unroll
+    for (int j = 0; j < 32 * T::ROW / 1024; ++j)
+      *(__attribute__((address_space(3))) u32x4*)(dg + j * 1024 + lane * 16) = dv[j];
+  }
+
+  // Seed rows: raw live diagonal score q_i . k_live_i, for the epilogue.
+  float s_live = 0.0f;
   if (wave_diag) {
     const int qr = min(qd0 + l32, L - 1);
     const uint32_t* krow = (const uint32_t*)(p.kl + kvoff + (int64_t)qr * p.kv_sl + hl * 8);
@@ -301,33 +391,30 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       }
     }
     s_live = swap_add(acc);
-    // live V rows of the block's queries, row-major, for the epilogue
-#pragma unroll
-    for (int i = 0; i < 32 * T::CH / 64; ++i) {
-      const int idx = lane + i * 64;
-      const int row = idx / T::CH, c = idx % T::CH;
-      const int vr = min(qd0 + row, L - 1);
-      lds_write16(dg + row * T::ROW + c * 16, *(const u32x4*)(p.vl + kvoff + (int64_t)vr * p.kv_sl + c * 8));
-    }
   }
 
-  // ---- pipeline prologue: K(seq 0), V(seq 0), K(seq 1) resident; S(seq 0) computed ---------
-  kstore(K0);
-  vstore(V0);
+  // ---- per-lane LDS read addresses (relative to a stage buffer) ---------------------------
+  uint32_t kaddr[T::KS];
 #pragma unroll
-  for (int j = 0; j < T::LOADS; ++j) kst[j] = kst1[j];
-  kstore(K1);
-  __syncthreads();
+  for (int ks = 0; ks < T::KS; ++ks) kaddr[ks] = k_off<T::ROW>(kp * 32 + l32, 2 * ks + hl);
+  // A operand of O^T += V^T P^T for keys kp*32 + 16*kk + {0..3, 8..11} + 4*(G/2), d-block db:
+  // lane (G = lane/16, i = lane%16) reads V[row][db*32 + 16*(G%2) + 4*(i%4) ..+3] with
+  // row = kp*32 + 16*kk + 4*(G/2) + i/4 (+8 for the upper half).  kk and the +8 move the row
+  // by multiples of 4, which leaves the swizzle unchanged: they are constant offsets.
+  uint32_t vaddr[T::DB];
+  {
+    const int G = lane >> 4, ii = lane & 15;
+    const int row = kp * 32 + 4 * (G >> 1) + (ii >> 2);
+#pragma unroll
+    for (int db = 0; db < T::DB; ++db) vaddr[db] = v_elem<T::ROW>(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
+  }
 
-  const float c2 = p.c2;
   auto qk = [&](const lds_t* kb, f32x16* s) {
-    s[0] = (f32x16){};
-    s[1] = (f32x16){};
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + k_off<T::ROW>(kp * 32 + l32, 2 * ks + hl)));
-      s[0] = mfma(a, qreg[0][ks], s[0]);
-      s[1] = mfma(a, qreg[1][ks], s[1]);
+      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
+      s[0] = mfma(a, qreg[0][ks], ks == 0 ? (f32x16){} : s[0]);
+      s[1] = mfma(a, qreg[1][ks], ks == 0 ? (f32x16){} : s[1]);
     }
   };
   // keys of this wave's tile of `stage` past L, and the seed rows' own (cached) column, get
@@ -351,14 +438,11 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       }
     }
   };
-  auto rowmax = [&](const f32x16* s, float* mt) {
+  auto lane_max = [&](const f32x16& s) -> float {
+    float x = fmax3(s[0], s[1], s[2]);
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      float mx = s[qb][0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmax2(mx, s[qb][r]);
-      mt[qb] = swap_max(mx) * c2;
-    }
+    for (int r = 3; r < 15; r += 2) x = fmax3(x, s[r], s[r + 1]);
+    return fmax2(x, s[15]);
   };
 
   float m[2], lsum[2] = {0.0f, 0.0f};
@@ -367,75 +451,135 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
     for (int db = 0; db < T::DB; ++db) o[qb][db] = (f32x16){};
-
-  f32x16 s_cur[2], s_nxt[2];
-  qk(K0, s_cur);
-  special_fix(seq(0), s_cur);
-  {
-    // the first tile fixes each row's reference max (no accumulator to rescale yet)
-    float mt[2];
-    rowmax(s_cur, mt);
-    m[0] = mt[0] > kInitMax ? mt[0] : kInitMax;
-    m[1] = mt[1] > kInitMax ? mt[1] : kInitMax;
-  }
-  __syncthreads();  // every wave has read K(seq 0) before iteration 0 overwrites its buffer
-
-  // softmax of S(seq i) into bf16 P (row sums accumulated), then O^T += V^T P^T
-  auto softmax_pv = [&](const lds_t* vcur) {
+  // softmax of S into bf16 P (row sums of the bf16 weights, as the MFMA sees them), then
+  // O^T += V^T P^T
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  auto softmax_pv = [&](const f32x16* s, const lds_t* vcur) {
     bf16x8 pk[2][2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const float nm = -m[qb];
       f32x16 pr;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[qb][r], c2, nm));
-      float ls = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) ls += pr[r];
-      lsum[qb] += ls;
+      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, nm));
       pk[qb][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
       pk[qb][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+      float ls = lsum[qb];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8 w = pk[qb][kk];
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, ls, false);
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, ls, false);
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, ls, false);
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, ls, false);
+      }
+      lsum[qb] = ls;
     }
+    typedef short i16x8 __attribute__((ext_vector_type(8)));
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
       for (int db = 0; db < T::DB; ++db) {
-        const bf16x8 a = v_operand<T::ROW>(vcur, kp * 32 + 16 * kk, db, lane);
+        const lds_t* base = vcur + vaddr[db] + kk * 16 * T::ROW;
+        const i16x8 v = __builtin_shufflevector(v_tr(base), v_tr(base + 8 * T::ROW), 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, v);
         o[0][db] = mfma(a, pk[0][kk], o[0][db]);
         o[1][db] = mfma(a, pk[1][kk], o[1][db]);
       }
     }
   };
 
-  // ---- steady state: regular stages, no masking, no diagonal, no rescale ----------------
-  // A row whose max grows by more than 2^kSlack over its reference leaves for the general
-  // loop below, which rescales.
-  int i = 0;
-  for (; i < n_reg; ++i) {
-    float mt[2];
-    rowmax(s_cur, mt);
-    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) || (mt[1] > m[1] + kSlack)) != 0) break;
-    gload(kst, p.kl, p.kc, seq(i + 2));
-    gload(vst, p.vl, p.vc, seq(i + 1));
-    qk((i & 1) ? K0 : K1, s_nxt);
-    softmax_pv((i & 1) ? V1 : V0);
-    kstore((i & 1) ? K1 : K0);        // K(seq i+2) replaces K(seq i)
-    vstore((i & 1) ? V0 : V1);  // V(seq i+1) replaces V(seq i-1)
-    __syncthreads();
-    s_cur[0] = s_nxt[0];
-    s_cur[1] = s_nxt[1];
+  // raw score above which a row leaves the branch-free steps: (m + slack) / c2 (c2 > 0)
+  float thr[2];
+  const float inv_c2 = 1.0f / c2;
+  auto set_thr = [&]() {
+    thr[0] = (m[0] + kSlack) * inv_c2;
+    thr[1] = (m[1] + kSlack) * inv_c2;
+  };
+  // true when every score of S is within the slack of its row's reference max
+  auto in_range = [&](const f32x16* s) -> bool {
+    const bool over = (lane_max(s[0]) > thr[0]) | (lane_max(s[1]) > thr[1]);
+    return __builtin_amdgcn_ballot_w64(over) == 0;
+  };
+
+  // ---- prologue ------------------------------------------------------------------------------
+  // K(0), V(0), K(1) go straight to their buffers; K(2) and V(1) wait in the staging
+  // registers for the first step.  Then S(0) and the reference row max.
+  u32x4 stgK[T::IPW], stgV[T::IPW];
+  {
+    u32x4 pre[3][T::IPW];
+    ld(pre[0], klb, kcb, offK, false, seq(0));
+    ld(pre[1], vlb, vcb, offV, true, seq(0));
+    ld(pre[2], klb, kcb, offK, false, seq(1));
+    ld(stgK, klb, kcb, offK, false, seq(2));
+    ld(stgV, vlb, vcb, offV, true, seq(1));
+    __builtin_amdgcn_s_waitcnt(T::kWaitPrev);  // the first three stages landed
+    st(pre[0], kbuf(0));
+    st(pre[1], vbuf(0));
+    st(pre[2], kbuf(1));
   }
-  // ---- general step: special tiles, and regular tiles after a rescale ------------------
-  auto general_step = [&](int i, bool special) {
-    const bool more = i + 1 < n_it;
-    if (more) {
-      gload(kst, p.kl, p.kc, seq(i + 2));
-      gload(vst, p.vl, p.vc, seq(i + 1));
-    }
-    if (special) special_fix(seq(i), s_cur);
+  __syncthreads();
+  f32x16 sA[2], sB[2];
+  qk(kbuf(0), sA);
+  if (n_reg == 0) special_fix(seq(0), sA);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const float mt = swap_max(lane_max(sA[qb])) * c2;
+    m[qb] = mt > kInitMax ? mt : kInitMax;
+  }
+  set_thr();
+  __builtin_amdgcn_s_barrier();  // every wave has read K(0) before its buffer is refilled
+
+  // ---- steady state ------------------------------------------------------------------------
+  // Step i (i-th stage processed): store the staged K(i+2) and V(i+1) (loaded during step
+  // i-1) into the buffers of K(i) and V(i-1), start the loads of K(i+3) and V(i+2);
+  // S(i+1) = K(i+1) Q^T; softmax of S(i) and O += P V(i).  Stage i uses K/V buffer i%2 and
+  // S buffer i%2, so two steps are unrolled with fixed buffers.  A row whose next scores
+  // exceed its reference max by more than 2^kSlack sends the remaining stages to the
+  // general step, which rescales before the exponentials.
+  int i = 0;
+  const int fast_end = min(n_reg, n_it - 1);
+  auto fast_step = [&](auto ph) -> bool {
+    constexpr int P = decltype(ph)::value;
+    f32x16* sc = P ? sB : sA;
+    f32x16* sn = P ? sA : sB;
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // K(i+2), V(i+1) staged
+    st(stgK, kbuf(P));
+    st(stgV, vbuf(P ^ 1));
+    ld(stgK, klb, kcb, offK, false, seq(i + 3));
+    ld(stgV, vlb, vcb, offV, true, seq(i + 2));
+    qk(kbuf(P ^ 1), sn);
+    softmax_pv(sc, vbuf(P));
+    const bool ok = in_range(sn);
+    step_schedule<T>();
+    __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(0));  // this step's LDS stores are complete
+    __builtin_amdgcn_s_barrier();
+    return ok;
+  };
+  while (i < fast_end) {
+    bool ok;
+    ok = fast_step(IC<0>{}); if (++i >= fast_end || !ok) break;
+    ok = fast_step(IC<1>{}); ++i;
+    if (!ok) break;
+  }
+  f32x16 s_cur[2], s_nxt[2];
+  s_cur[0] = (i & 1) ? sB[0] : sA[0];
+  s_cur[1] = (i & 1) ? sB[1] : sA[1];
+
+  // ---- general step: special stages, the last stage, every stage after a rescale ---------
+  for (; i < n_it; ++i) {
+    const int r = i & 1;
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    st(stgK, kbuf(r));
+    st(stgV, vbuf(r ^ 1));
+    ld(stgK, klb, kcb, offK, false, seq(i + 3));
+    ld(stgV, vlb, vcb, offV, true, seq(i + 2));
+    if (i >= n_reg) special_fix(seq(i), s_cur);
     float mt[2];
-    rowmax(s_cur, mt);
-    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) || (mt[1] > m[1] + kSlack)) != 0) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) mt[qb] = swap_max(lane_max(s_cur[qb])) * c2;
+    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) | (mt[1] > m[1] + kSlack)) != 0) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const float mn = mt[qb] > m[qb] + kSlack ? mt[qb] : m[qb];
@@ -446,41 +590,34 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
         for (int db = 0; db < T::DB; ++db) o[qb][db] *= alpha;
       }
     }
-    if (more) qk((i & 1) ? K0 : K1, s_nxt);
-    softmax_pv((i & 1) ? V1 : V0);
-    if (more) {
-      kstore((i & 1) ? K1 : K0);
-      vstore((i & 1) ? V0 : V1);
-    }
-    __syncthreads();
+    if (i + 1 < n_it) qk(kbuf(r ^ 1), s_nxt);
+    softmax_pv(s_cur, vbuf(r));
+    __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(0));
+    __builtin_amdgcn_s_barrier();
     s_cur[0] = s_nxt[0];
     s_cur[1] = s_nxt[1];
-  };
-  // regular stages left after a rescale (rare)
-  for (; i < n_reg; ++i) general_step(i, false);
-  // the (at most three) special stages, straight-line
-#pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    if (i < n_it) {
-      general_step(i, true);
-      ++i;
-    }
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __syncthreads();
 
   // ---- merge the two key parities, add the live diagonal term, normalise, store ---------
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) lsum[qb] = swap_add(lsum[qb]);
-  // Wave kp finalises its query block kp; the other block goes to the partner wave (w ^ 2).
-  // Register arrays are indexed with compile-time block numbers only.
-  float* mine = (float*)(smem_raw + wave * T::MERGE);
-  const float* theirs = (const float*)(smem_raw + (wave ^ 2) * T::MERGE);
-  constexpr int NJ = T::DB * 16;
+  // Wave kp finalises its query block kp; the other block goes to the partner wave (w ^ 2)
+  // through LDS (each wave's slot is one stage buffer; m and l separately).  Register arrays
+  // are indexed with compile-time block numbers only.
+  auto slot = [&](int w) -> float* {
+    return (float*)(w == 0 ? sK0 : (w == 1 ? sK1 : (w == 2 ? sV0 : sV1)));
+  };
+  float* mine = slot(wave);
+  const float* theirs = slot(wave ^ 2);
+  constexpr int NJ = T::NJ;
   auto give = [&](auto qo) {
     constexpr int QO = decltype(qo)::value;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) mine[j * 64 + lane] = o[QO][j >> 4][j & 15];
-    mine[NJ * 64 + lane] = m[QO];
-    mine[(NJ + 1) * 64 + lane] = lsum[QO];
+    sML[(wave * 2 + 0) * 64 + lane] = m[QO];
+    sML[(wave * 2 + 1) * 64 + lane] = lsum[QO];
   };
   if (kp) give(IC<0>{}); else give(IC<1>{});
   __syncthreads();
@@ -489,8 +626,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     // seed rows: the live diagonal term, one more element of the row's softmax
     const float td = qd_seed ? s_live * c2 : -INFINITY;
     const float ma = m[QF], la = lsum[QF];
-    const float mb = theirs[NJ * 64 + lane], lb = theirs[(NJ + 1) * 64 + lane];
-    const float mm = fmax2(fmax2(ma, mb), td);
+    const float mb = sML[((wave ^ 2) * 2 + 0) * 64 + lane], lb = sML[((wave ^ 2) * 2 + 1) * 64 + lane];
+    const float mm = fmax3(ma, mb, td);
     const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
     const float fd = __builtin_amdgcn_exp2f(td - mm);
     const float ltot = la * fa + lb * fb + fd;
@@ -511,7 +648,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
           }
           if (wave_diag) {
             typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-            const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(dg + l32 * T::ROW + d0 * 2);
+            const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
+                dg + l32 * T::ROW + ((((d0 >> 3) ^ k_swz<T::ROW>(l32))) << 4) + (d0 & 7) * 2);
             v[0] += fd * bf16_lo(raw[0]);
             v[1] += fd * bf16_hi(raw[0]);
             v[2] += fd * bf16_lo(raw[1]);
