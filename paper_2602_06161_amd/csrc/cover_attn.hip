@@ -50,7 +50,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) char lds_t;
 typedef __attribute__((address_space(1))) const char gmem_t;  // global memory, read-only here
 
-constexpr int kThreads = 256;
+constexpr int kWaves = 8;             // waves per workgroup: two per SIMD
+constexpr int kThreads = 64 * kWaves;
 constexpr int kBM = 128;             // queries per workgroup
 constexpr int kStageKeys = 64;       // keys per pipeline stage = two 32-key wave tiles
 constexpr float kSlack = 20.0f;      // rescale only when a row max grows by > 2^20
@@ -63,17 +64,17 @@ constexpr int lgkmcnt_imm(int n) { return 0xf | (3 << 14) | 0x70 | ((n & 15) << 
 
 template <int D>
 struct Tile {
-  static constexpr int CH = D / 8;                  // 16-byte chunks per bf16 row
-  static constexpr int KS = D / 16;                 // k-steps of S^T = K Q^T
-  static constexpr int DB = D / 32;                 // 32-row blocks of O^T
-  static constexpr int ROW = D * 2;                 // bytes per row
-  static constexpr int SBYTES = kStageKeys * ROW;   // one K or V stage of 64 rows
-  static constexpr int RPI = 1024 / ROW;            // rows per 1-KiB direct-to-LDS wave load
-  static constexpr int IPW = SBYTES / 1024 / 4;     // such loads per wave per stage
-  static constexpr int NJ = DB * 16;                // O^T values per lane per query block
-  // s_waitcnt immediate: at most 2*IPW vector-memory loads outstanding
+  static constexpr int CH = D / 8;                     // 16-byte chunks per bf16 row
+  static constexpr int KS = D / 16;                    // k-steps of S^T = K Q^T
+  static constexpr int DB = D / 32;                    // 32-row blocks of O^T
+  static constexpr int ROW = D * 2;                    // bytes per row
+  static constexpr int SBYTES = kStageKeys * ROW;      // one K or V stage of 64 rows
+  static constexpr int RPI = 1024 / ROW;               // rows per 1-KiB wave load
+  static constexpr int IPW = SBYTES / 1024 / kWaves;   // such loads per wave per stage
+  static constexpr int NJH = DB / 2 * 16;              // O^T values per lane in half of d
   static constexpr int kWaitPrev = vmcnt_imm(2 * IPW);
-  static_assert(NJ * 64 * 4 <= SBYTES, "a wave's merge slot must fit one stage buffer");
+  static_assert(IPW >= 1, "a stage must give every wave at least one load");
+  static_assert(2 * NJH * 64 * 4 <= SBYTES, "two merge slots must fit one stage buffer");
 };
 
 struct Params {
@@ -142,63 +143,27 @@ struct IC {
   static constexpr int value = N;
 };
 
-// 16-byte direct global -> LDS load: lane l's bytes land at dst + 16 l.
-__device__ __forceinline__ void dma16(const void* src, lds_t* dst) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
-}
-
-// Instruction order of one branch-free pipeline step (one wave issues in order, so the
-// matrix core stays busy only if vector work is threaded between the MFMAs): K operand
-// reads, a few exponentials to cover their latency, the S = K Q^T MFMAs each followed by
-// softmax work, the V operand reads, then the PV MFMAs each followed by the remaining
-// vector work (next tile's copies and range check, row sums).
-template <class T>
-__device__ __forceinline__ void step_schedule() {
-  constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
-  constexpr int nqk = 2 * T::KS, npv = 4 * T::DB;
-  __builtin_amdgcn_sched_group_barrier(kDsRead, T::KS, 0);
-  __builtin_amdgcn_sched_group_barrier(kValu, 6, 0);
-#pragma unroll
-  for (int k = 0; k < nqk / 2; ++k) {
-    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * 2 * T::DB, 0);
-#pragma unroll
-  for (int k = 0; k < nqk / 2; ++k) {
-    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
-  }
-#pragma unroll
-  for (int k = 0; k < npv; ++k) {
-    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kValu, 4, 0);
-  }
-}
-
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Params p) {
   using T = Tile<D>;
-  // Two K and two V stage buffers; the loads for a stage are staged in registers one step
-  // ahead.
+  // Two K and two V stage buffers (the loads of a stage are staged in registers one step
+  // ahead), the live value rows of the seed rows' diagonals, merge scalars, seed bitmap.
   __shared__ __attribute__((aligned(1024))) char sK0[T::SBYTES];
   __shared__ __attribute__((aligned(1024))) char sK1[T::SBYTES];
   __shared__ __attribute__((aligned(1024))) char sV0[T::SBYTES];
   __shared__ __attribute__((aligned(1024))) char sV1[T::SBYTES];
-  __shared__ __attribute__((aligned(1024))) char sDiag0[32 * T::ROW];
-  __shared__ __attribute__((aligned(1024))) char sDiag1[32 * T::ROW];
-  __shared__ __attribute__((aligned(1024))) char sDiag2[32 * T::ROW];
-  __shared__ __attribute__((aligned(1024))) char sDiag3[32 * T::ROW];
-  __shared__ __attribute__((aligned(16))) float sML[4 * 2 * 64];
+  __shared__ __attribute__((aligned(1024))) char sDiag[4 * 32 * T::ROW];
+  __shared__ __attribute__((aligned(16))) float sML[kWaves * 2 * 64];
   __shared__ uint32_t bits[COVER_MAX_L / 32];
+  __shared__ uint32_t sdirty[COVER_MAX_L / kStageKeys / 32];  // stages holding a seed
   auto kbuf = [&](int n) -> lds_t* { return (lds_t*)(n == 0 ? sK0 : sK1); };
   auto vbuf = [&](int n) -> lds_t* { return (lds_t*)(n == 0 ? sV0 : sV1); };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qh = wave & 1;   // which 64-query half of the workgroup tile
-  const int kp = wave >> 1;  // which key parity (32-key tile kp of every 64-key stage)
+  const int qq = wave & 3;   // 32-query block of the workgroup tile
+  const int kp = wave >> 2;  // key half: 32-key tile kp of every 64-key stage
   const int hl = lane >> 5, l32 = lane & 31;
 
   // ---- workgroup -> (b, h, query tile); consecutive logical tiles share an XCD --------
@@ -210,84 +175,66 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   const int g = h / p.group;
   const int L = p.L;
   const int q0 = qt * kBM;
+  const int qw = q0 + qq * 32;  // this wave's first query
   const __bf16* qbase = p.q + b * p.q_sb + h * p.q_sh;
   const int64_t kvoff = b * p.kv_sb + g * p.kv_sh;
-
-  // ---- Q fragments (B operand of S^T = K Q^T): query l32 of block qb, d-chunk 2*ks + hl
   const float c2 = p.c2;
-  bf16x8 qreg[2][T::KS];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int qi = min(q0 + qh * 64 + qb * 32 + l32, L - 1);
+
+  // ---- Q fragments (B operand of S^T = K Q^T): query qw + l32, d-chunk 2*ks + hl ---------
+  bf16x8 qreg[T::KS];
+  {
+    const int qi = min(qw + l32, L - 1);
     const __bf16* qrow = qbase + (int64_t)qi * p.q_sl + hl * 8;
 #pragma unroll
-    for (int ks = 0; ks < T::KS; ++ks) qreg[qb][ks] = *(const bf16x8*)(qrow + ks * 16);
+    for (int ks = 0; ks < T::KS; ++ks) qreg[ks] = *(const bf16x8*)(qrow + ks * 16);
   }
 
   // ---- seed bitmap of this sequence ---------------------------------------------------
-  // The seed list is read speculatively (all max_seeds entries) together with its length.
+  // The seed list is read speculatively (the first kThreads entries) with its length.
   const int nwords = (L + 31) >> 5;
+  const int n_it = (L + kStageKeys - 1) / kStageKeys;
   const int64_t sbase = (int64_t)b * p.max_seeds;
   int ns = 0;
   if (p.max_seeds > 0) ns = p.n_seed[b];
   const int sj0 = tid < p.max_seeds ? p.seed_idx[sbase + tid] : -1;
   // words past the sequence are cleared too: per-stage lookups read two words per stage
-  for (int w = tid; w < 2 * ((L + kStageKeys - 1) / kStageKeys); w += kThreads) bits[w] = 0u;
+  for (int w = tid; w < 2 * n_it; w += kThreads) bits[w] = 0u;
+  if (tid < COVER_MAX_L / kStageKeys / 32) sdirty[tid] = 0u;
   __syncthreads();
   ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
-  if (tid < ns && (unsigned)sj0 < (unsigned)L) atomicOr(&bits[sj0 >> 5], 1u << (sj0 & 31));
+  auto mark = [&](int j) {
+    atomicOr(&bits[j >> 5], 1u << (j & 31));
+    atomicOr(&sdirty[j >> 11], 1u << ((j >> 6) & 31));
+  };
+  if (tid < ns && (unsigned)sj0 < (unsigned)L) mark(sj0);
   for (int t = tid + kThreads; t < ns; t += kThreads) {
     const int j = p.seed_idx[sbase + t];
-    if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
+    if ((unsigned)j < (unsigned)L) mark(j);
   }
   __syncthreads();
   auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
 
-  // ---- stage order ---------------------------------------------------------------------
-  // Stages of 64 keys.  Up to three need per-element care -- the two holding this tile's
-  // diagonal when the tile has seeds, and a ragged last stage -- and are processed last, so
-  // every earlier stage runs through one branch-free step.
-  const int n_it = (L + kStageKeys - 1) / kStageKeys;
-  constexpr int kNone = 0x7fffffff;
+  // ---- stages ----------------------------------------------------------------------------
+  // Stages of 64 keys are processed in order.  Up to three need per-element care: the two
+  // holding this tile's diagonal when the tile has seeds, and a ragged last stage.
   uint32_t tile_bits = 0;
 #pragma unroll
   for (int w = 0; w < kBM / 32; ++w) tile_bits |= (q0 / 32 + w < nwords) ? bits[q0 / 32 + w] : 0u;
   const bool tile_seeded = __builtin_amdgcn_readfirstlane(tile_bits) != 0u;
-  const int spC = __builtin_amdgcn_readfirstlane(L % kStageKeys != 0 ? n_it - 1 : -1);  // ragged
-  // the special stages in increasing order (kNone when absent)
-  int sp0 = tile_seeded ? 2 * qt : kNone;
-  int sp1 = (tile_seeded && 2 * qt + 1 < n_it) ? 2 * qt + 1 : kNone;
-  int sp2 = (spC >= 0 && spC != sp0 && spC != sp1) ? spC : kNone;
-  if (sp0 == kNone) { sp0 = sp1; sp1 = sp2; sp2 = kNone; }
-  if (sp0 == kNone) { sp0 = sp1; sp1 = kNone; }
-  if (sp1 == kNone) { sp1 = sp2; sp2 = kNone; }
-  sp0 = __builtin_amdgcn_readfirstlane(sp0);
-  sp1 = __builtin_amdgcn_readfirstlane(sp1);
-  sp2 = __builtin_amdgcn_readfirstlane(sp2);
-  const int n_reg = n_it - (sp0 != kNone) - (sp1 != kNone) - (sp2 != kNone);
-  // stage processed at position i (positions past the end repeat the last one)
-  auto seq = [=](int i) -> int {
-    if (i >= n_it) i = n_it - 1;
-    if (i >= n_reg) {
-      const int k = i - n_reg;
-      return k == 0 ? sp0 : (k == 1 ? sp1 : sp2);
-    }
-    // regular position i skips the special stages: j >= s  <=>  s - 1 - j < 0
-    int j = i;
-    j += (int)((uint32_t)(sp0 - 1 - j) >> 31);
-    j += (int)((uint32_t)(sp1 - 1 - j) >> 31);
-    j += (int)((uint32_t)(sp2 - 1 - j) >> 31);
-    return __builtin_amdgcn_readfirstlane(j);
-  };
-  // stages 0..63 holding a seed, one bit each (later stages consult the bitmap)
-  const uint64_t dirty64 = __builtin_amdgcn_ballot_w64(
-      2 * lane < nwords && (bits[2 * lane] | (2 * lane + 1 < nwords ? bits[2 * lane + 1] : 0u)) != 0u);
+  const int spA = tile_seeded ? 2 * qt : -1;
+  const int spB = tile_seeded ? 2 * qt + 1 : -1;
+  const int spC = L % kStageKeys != 0 ? n_it - 1 : -1;  // ragged
+  auto is_special = [=](int i) -> bool { return (i == spA) | (i == spB) | (i == spC); };
+  // Lane l holds the seed flags of stages 64l .. 64l+63 (two words); a stage's flag is read
+  // back with a lane read, no memory access.
+  const uint32_t dirty_lo = sdirty[(2 * lane) & (COVER_MAX_L / kStageKeys / 32 - 1)];
+  const uint32_t dirty_hi = sdirty[(2 * lane + 1) & (COVER_MAX_L / kStageKeys / 32 - 1)];
   auto dirty = [&](int stage) -> bool {
-    if (stage < 64) return (dirty64 >> stage) & 1u;
-    const uint32_t w0 = __builtin_amdgcn_readfirstlane(bits[2 * stage]);
-    const uint32_t w1 = __builtin_amdgcn_readfirstlane(bits[2 * stage + 1]);
-    return (w0 | w1) != 0u;
+    const uint32_t w = ((stage >> 5) & 1) ? __builtin_amdgcn_readlane(dirty_hi, stage >> 6)
+                                          : __builtin_amdgcn_readlane(dirty_lo, stage >> 6);
+    return (w >> (stage & 31)) & 1u;
   };
+  auto clamp_stage = [=](int i) -> int { return i < n_it ? i : n_it - 1; };
 
   // ---- stage loads -------------------------------------------------------------------------
   // A stage is 64 rows; each wave moves IPW KiB of it, 16 bytes per lane per KiB, through
@@ -318,10 +265,10 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   gmem_t* const kcb = uniform_ptr(p.kc + kvoff);
   gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
   gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
-  // Issue the loads of one stage (64 rows) of K or V into st[0..IPW).  Stages without seeds
-  // and within L use a scalar base and per-lane 32-bit offsets; the others choose each row's
-  // source and clamp rows past L.
   typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+  // Issue the loads of one stage of K or V into st[0..IPW).  Stages without seeds and within
+  // L use a scalar base and per-lane 32-bit offsets; the others choose each row's source and
+  // clamp rows past L.
   auto ld = [&](u32x4* st, gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v,
                 int stage_in) {
     const int stage = __builtin_amdgcn_readfirstlane(stage_in);
@@ -339,51 +286,48 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       }
     }
   };
-  lds_t* const lds_slot = (lds_t*)nullptr + wave * (T::IPW * 1024) + lane * 16;  // within a buffer
+  const uint32_t lds_slot = wave * (T::IPW * 1024) + lane * 16;  // within a stage buffer
   auto st = [&](const u32x4* stg, lds_t* buf) {
 #pragma unroll
-    for (int j = 0; j < T::IPW; ++j)
-      *(__attribute__((address_space(3))) u32x4*)(buf + (uintptr_t)lds_slot + j * 1024) = stg[j];
+    for (int j = 0; j < T::IPW; ++j) *(__attribute__((address_space(3))) u32x4*)(buf + lds_slot + j * 1024) = stg[j];
   };
 
   // ---- diagonal set-up ------------------------------------------------------------------
-  // Query block kp of this wave (queries qd0 .. qd0+31) has its diagonal in this wave's
-  // 32-key tile of stage itd = qd0 / 64.  In S^T the diagonal entry of query nq sits in lane
-  // half (nq/4)%2, register (nq/8)*4 + nq%4.
-  const int qd0 = q0 + qh * 64 + kp * 32;
-  const int itd = qd0 / kStageKeys;
+  // Query c of this wave (position qw + c) has its diagonal key at position qw + c, which
+  // lies in this wave's key tile exactly when kp == qq % 2, in stage itd = qw / 64.  In S^T
+  // the diagonal entry of query c sits in lane half (c/4)%2, register (c/8)*4 + c%4.
+  const bool diag_wave = kp == (qq & 1);
+  const int itd = qw / kStageKeys;
   const bool holds_diag = hl == ((l32 >> 2) & 1);
   const int rd = ((l32 >> 3) << 2) | (l32 & 3);
-  const bool qd_seed = (qd0 + l32) < L && is_seed(qd0 + l32);  // this lane's diagonal query
-  const bool diag_seed = holds_diag && qd_seed;
-  const bool wave_diag = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
-
+  const bool qd_seed = (qw + l32) < L && is_seed(qw + l32);  // this lane's query is a seed
+  const bool diag_seed = diag_wave && holds_diag && qd_seed;
+  const bool block_seeded = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
   // Seed rows need the live value row of their own position in the epilogue: the 32 rows
-  // of this wave's diagonal block go to its sDiag slot (K swizzle).
-  lds_t* const dg = (lds_t*)(wave == 0 ? sDiag0 : (wave == 1 ? sDiag1 : (wave == 2 ? sDiag2 : sDiag3)));
-  if (wave_diag) {
-    u32x4 dv[32 * T::ROW / 1024];
+  // of each query block go to its sDiag slot (K swizzle), loaded by the block's diagonal wave.
+  lds_t* const dg = (lds_t*)sDiag + qq * (32 * T::ROW);
+  if (block_seeded && diag_wave) {
+    constexpr int NL = 32 * T::ROW / 1024;
+    u32x4 dv[NL];
 #pragma unroll
-    for (int j = 0; j < 32 * T::ROW / 1024; ++j) {
+    for (int j = 0; j < NL; ++j) {
       const int row = j * T::RPI + lane / T::CH, pc = lane % T::CH;
-      const int vr = min(qd0 + row, L - 1);
+      const int vr = min(qw + row, L - 1);
       dv[j] = *(gu32x4*)(vlb + vr * row_bytes + ((pc ^ k_swz<T::ROW>(row)) << 4));
     }
 #pragma unroll
-    for (int j = 0; j < 32 * T::ROW / 1024; ++j)
-      *(__attribute__((address_space(3))) u32x4*)(dg + j * 1024 + lane * 16) = dv[j];
+    for (int j = 0; j < NL; ++j) *(__attribute__((address_space(3))) u32x4*)(dg + j * 1024 + lane * 16) = dv[j];
   }
-
-  // Seed rows: raw live diagonal score q_i . k_live_i, for the epilogue.
+  // Seed rows: raw live diagonal score q_i . k_live_i (both waves of the block need it).
   float s_live = 0.0f;
-  if (wave_diag) {
-    const int qr = min(qd0 + l32, L - 1);
+  if (block_seeded) {
+    const int qr = min(qw + l32, L - 1);
     const uint32_t* krow = (const uint32_t*)(p.kl + kvoff + (int64_t)qr * p.kv_sl + hl * 8);
     float acc = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks) {
       const u32x4 kv = *(const u32x4*)(krow + ks * 8);
-      const u32x4 qv = __builtin_bit_cast(u32x4, kp ? qreg[1][ks] : qreg[0][ks]);
+      const u32x4 qv = __builtin_bit_cast(u32x4, qreg[ks]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
@@ -399,8 +343,9 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   for (int ks = 0; ks < T::KS; ++ks) kaddr[ks] = k_off<T::ROW>(kp * 32 + l32, 2 * ks + hl);
   // A operand of O^T += V^T P^T for keys kp*32 + 16*kk + {0..3, 8..11} + 4*(G/2), d-block db:
   // lane (G = lane/16, i = lane%16) reads V[row][db*32 + 16*(G%2) + 4*(i%4) ..+3] with
-  // row = kp*32 + 16*kk + 4*(G/2) + i/4 (+8 for the upper half).  kk and the +8 move the row
-  // by multiples of 4, which leaves the swizzle unchanged: they are constant offsets.
+  // row = kp*32 + 16*kk + 4*(G/2) + i/4 (+8 for the upper half).  The same key order is
+  // what the S^T registers give the P^T operand.  kk and the +8 move the row by multiples
+  // of 4, which leaves the swizzle unchanged: they are constant offsets.
   uint32_t vaddr[T::DB];
   {
     const int G = lane >> 4, ii = lane & 15;
@@ -409,33 +354,27 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     for (int db = 0; db < T::DB; ++db) vaddr[db] = v_elem<T::ROW>(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
   }
 
-  auto qk = [&](const lds_t* kb, f32x16* s) {
+  auto qk = [&](const lds_t* kb, f32x16& s) {
 #pragma unroll
     for (int ks = 0; ks < T::KS; ++ks) {
       const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
-      s[0] = mfma(a, qreg[0][ks], ks == 0 ? (f32x16){} : s[0]);
-      s[1] = mfma(a, qreg[1][ks], ks == 0 ? (f32x16){} : s[1]);
+      s = mfma(a, qreg[ks], ks == 0 ? (f32x16){} : s);
     }
   };
   // keys of this wave's tile of `stage` past L, and the seed rows' own (cached) column, get
   // no weight; the live diagonal term is added in the epilogue
-  auto special_fix = [&](int stage, f32x16* s) {
+  auto special_fix = [&](int stage, f32x16& s) {
     if (stage * kStageKeys + kStageKeys > L) {
       const int kbase = stage * kStageKeys + kp * 32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const bool ok = kbase + ((r >> 2) << 3) + hl * 4 + (r & 3) < L;
-        s[0][r] = ok ? s[0][r] : -INFINITY;
-        s[1][r] = ok ? s[1][r] : -INFINITY;
+        s[r] = ok ? s[r] : -INFINITY;
       }
     }
-    if (wave_diag && stage == itd) {
+    if (diag_wave && block_seeded && stage == itd) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool hit = diag_seed && r == rd;
-        s[0][r] = (hit && kp == 0) ? -INFINITY : s[0][r];
-        s[1][r] = (hit && kp == 1) ? -INFINITY : s[1][r];
-      }
+      for (int r = 0; r < 16; ++r) s[r] = (diag_seed && r == rd) ? -INFINITY : s[r];
     }
   };
   auto lane_max = [&](const f32x16& s) -> float {
@@ -445,37 +384,35 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     return fmax2(x, s[15]);
   };
 
-  float m[2], lsum[2] = {0.0f, 0.0f};
-  f32x16 o[2][T::DB];
+  float m, lsum = 0.0f, thr;
+  f32x16 o[T::DB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int db = 0; db < T::DB; ++db) o[qb][db] = (f32x16){};
+  for (int db = 0; db < T::DB; ++db) o[db] = (f32x16){};
+  // raw score above which a row leaves the branch-free steps: (m + slack) / c2 (c2 > 0)
+  const float inv_c2 = 1.0f / c2;
+
   // softmax of S into bf16 P (row sums of the bf16 weights, as the MFMA sees them), then
   // O^T += V^T P^T
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  auto softmax_pv = [&](const f32x16* s, const lds_t* vcur) {
-    bf16x8 pk[2][2];
+  auto softmax_pv = [&](const f32x16& s, const lds_t* vcur) {
+    const float nm = -m;
+    f32x16 pr;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const float nm = -m[qb];
-      f32x16 pr;
+    for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c2, nm));
+    bf16x8 pk[2];
+    pk[0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
+    pk[1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+    float ls = lsum;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, nm));
-      pk[qb][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
-      pk[qb][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
-      float ls = lsum[qb];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 w = pk[qb][kk];
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, ls, false);
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, ls, false);
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, ls, false);
-        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, ls, false);
-      }
-      lsum[qb] = ls;
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 w = pk[kk];
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, ls, false);
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, ls, false);
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, ls, false);
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, ls, false);
     }
+    lsum = ls;
     typedef short i16x8 __attribute__((ext_vector_type(8)));
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -483,24 +420,9 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       for (int db = 0; db < T::DB; ++db) {
         const lds_t* base = vcur + vaddr[db] + kk * 16 * T::ROW;
         const i16x8 v = __builtin_shufflevector(v_tr(base), v_tr(base + 8 * T::ROW), 0, 1, 2, 3, 4, 5, 6, 7);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, v);
-        o[0][db] = mfma(a, pk[0][kk], o[0][db]);
-        o[1][db] = mfma(a, pk[1][kk], o[1][db]);
+        o[db] = mfma(__builtin_bit_cast(bf16x8, v), pk[kk], o[db]);
       }
     }
-  };
-
-  // raw score above which a row leaves the branch-free steps: (m + slack) / c2 (c2 > 0)
-  float thr[2];
-  const float inv_c2 = 1.0f / c2;
-  auto set_thr = [&]() {
-    thr[0] = (m[0] + kSlack) * inv_c2;
-    thr[1] = (m[1] + kSlack) * inv_c2;
-  };
-  // true when every score of S is within the slack of its row's reference max
-  auto in_range = [&](const f32x16* s) -> bool {
-    const bool over = (lane_max(s[0]) > thr[0]) | (lane_max(s[1]) > thr[1]);
-    return __builtin_amdgcn_ballot_w64(over) == 0;
   };
 
   // ---- prologue ------------------------------------------------------------------------------
@@ -509,50 +431,49 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   u32x4 stgK[T::IPW], stgV[T::IPW];
   {
     u32x4 pre[3][T::IPW];
-    ld(pre[0], klb, kcb, offK, false, seq(0));
-    ld(pre[1], vlb, vcb, offV, true, seq(0));
-    ld(pre[2], klb, kcb, offK, false, seq(1));
-    ld(stgK, klb, kcb, offK, false, seq(2));
-    ld(stgV, vlb, vcb, offV, true, seq(1));
+    ld(pre[0], klb, kcb, offK, false, 0);
+    ld(pre[1], vlb, vcb, offV, true, 0);
+    ld(pre[2], klb, kcb, offK, false, clamp_stage(1));
+    ld(stgK, klb, kcb, offK, false, clamp_stage(2));
+    ld(stgV, vlb, vcb, offV, true, clamp_stage(1));
     __builtin_amdgcn_s_waitcnt(T::kWaitPrev);  // the first three stages landed
     st(pre[0], kbuf(0));
     st(pre[1], vbuf(0));
     st(pre[2], kbuf(1));
   }
   __syncthreads();
-  f32x16 sA[2], sB[2];
+  f32x16 sA, sB;
   qk(kbuf(0), sA);
-  if (n_reg == 0) special_fix(seq(0), sA);
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const float mt = swap_max(lane_max(sA[qb])) * c2;
-    m[qb] = mt > kInitMax ? mt : kInitMax;
+  if (is_special(0)) special_fix(0, sA);
+  {
+    const float mt = swap_max(lane_max(sA)) * c2;
+    m = mt > kInitMax ? mt : kInitMax;
+    thr = (m + kSlack) * inv_c2;
   }
-  set_thr();
   __builtin_amdgcn_s_barrier();  // every wave has read K(0) before its buffer is refilled
 
   // ---- steady state ------------------------------------------------------------------------
-  // Step i (i-th stage processed): store the staged K(i+2) and V(i+1) (loaded during step
-  // i-1) into the buffers of K(i) and V(i-1), start the loads of K(i+3) and V(i+2);
-  // S(i+1) = K(i+1) Q^T; softmax of S(i) and O += P V(i).  Stage i uses K/V buffer i%2 and
-  // S buffer i%2, so two steps are unrolled with fixed buffers.  A row whose next scores
-  // exceed its reference max by more than 2^kSlack sends the remaining stages to the
-  // general step, which rescales before the exponentials.
+  // Step i: store the staged K(i+2) and V(i+1) (loaded during step i-1) into the buffers of
+  // K(i) and V(i-1), start the loads of K(i+3) and V(i+2); S(i+1) = K(i+1) Q^T; softmax of
+  // S(i) and O += P V(i).  Stage i uses K/V buffer i%2 and S buffer i%2, so two steps are
+  // unrolled with fixed buffers.  A row whose next scores exceed its reference max by more
+  // than 2^kSlack sends the remaining stages to the general step, which rescales before the
+  // exponentials.
   int i = 0;
-  const int fast_end = min(n_reg, n_it - 1);
+  const int fast_end = n_it - 1;
   auto fast_step = [&](auto ph) -> bool {
     constexpr int P = decltype(ph)::value;
-    f32x16* sc = P ? sB : sA;
-    f32x16* sn = P ? sA : sB;
+    f32x16& sc = P ? sB : sA;
+    f32x16& sn = P ? sA : sB;
+    if (is_special(i)) special_fix(i, sc);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // K(i+2), V(i+1) staged
     st(stgK, kbuf(P));
     st(stgV, vbuf(P ^ 1));
-    ld(stgK, klb, kcb, offK, false, seq(i + 3));
-    ld(stgV, vlb, vcb, offV, true, seq(i + 2));
+    ld(stgK, klb, kcb, offK, false, clamp_stage(i + 3));
+    ld(stgV, vlb, vcb, offV, true, clamp_stage(i + 2));
     qk(kbuf(P ^ 1), sn);
     softmax_pv(sc, vbuf(P));
-    const bool ok = in_range(sn);
-    step_schedule<T>();
+    const bool ok = __builtin_amdgcn_ballot_w64(lane_max(sn) > thr) == 0;
     __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(0));  // this step's LDS stores are complete
     __builtin_amdgcn_s_barrier();
     return ok;
@@ -563,90 +484,85 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     ok = fast_step(IC<1>{}); ++i;
     if (!ok) break;
   }
-  f32x16 s_cur[2], s_nxt[2];
-  s_cur[0] = (i & 1) ? sB[0] : sA[0];
-  s_cur[1] = (i & 1) ? sB[1] : sA[1];
+  f32x16 s_cur = (i & 1) ? sB : sA, s_nxt;
 
-  // ---- general step: special stages, the last stage, every stage after a rescale ---------
+  // ---- general step: the last stage, and every stage after a rescale ----------------------
   for (; i < n_it; ++i) {
     const int r = i & 1;
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     st(stgK, kbuf(r));
     st(stgV, vbuf(r ^ 1));
-    ld(stgK, klb, kcb, offK, false, seq(i + 3));
-    ld(stgV, vlb, vcb, offV, true, seq(i + 2));
-    if (i >= n_reg) special_fix(seq(i), s_cur);
-    float mt[2];
+    ld(stgK, klb, kcb, offK, false, clamp_stage(i + 3));
+    ld(stgV, vlb, vcb, offV, true, clamp_stage(i + 2));
+    if (is_special(i)) special_fix(i, s_cur);
+    const float mt = swap_max(lane_max(s_cur)) * c2;
+    if (__builtin_amdgcn_ballot_w64(mt > m + kSlack) != 0) {
+      const float mn = mt > m + kSlack ? mt : m;
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);
+      m = mn;
+      thr = (m + kSlack) * inv_c2;
+      lsum *= alpha;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) mt[qb] = swap_max(lane_max(s_cur[qb])) * c2;
-    if (__builtin_amdgcn_ballot_w64((mt[0] > m[0] + kSlack) | (mt[1] > m[1] + kSlack)) != 0) {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const float mn = mt[qb] > m[qb] + kSlack ? mt[qb] : m[qb];
-        const float alpha = __builtin_amdgcn_exp2f(m[qb] - mn);
-        m[qb] = mn;
-        lsum[qb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < T::DB; ++db) o[qb][db] *= alpha;
-      }
+      for (int db = 0; db < T::DB; ++db) o[db] *= alpha;
     }
     if (i + 1 < n_it) qk(kbuf(r ^ 1), s_nxt);
     softmax_pv(s_cur, vbuf(r));
     __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(0));
     __builtin_amdgcn_s_barrier();
-    s_cur[0] = s_nxt[0];
-    s_cur[1] = s_nxt[1];
+    s_cur = s_nxt;
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
 
-  // ---- merge the two key parities, add the live diagonal term, normalise, store ---------
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) lsum[qb] = swap_add(lsum[qb]);
-  // Wave kp finalises its query block kp; the other block goes to the partner wave (w ^ 2)
-  // through LDS (each wave's slot is one stage buffer; m and l separately).  Register arrays
-  // are indexed with compile-time block numbers only.
+  // ---- merge the two key halves, add the live diagonal term, normalise, store -----------
+  // Waves w and w^4 hold the same 32 queries over the two key halves.  Wave kp finalises the
+  // d-half kp; the other half of its O^T goes to the partner through LDS (slot per wave,
+  // two slots per stage buffer; m and l separately).  Register arrays are indexed with
+  // compile-time numbers only.
+  lsum = swap_add(lsum);
+  constexpr int NJH = T::NJH;
+  constexpr int DBH = T::DB / 2;
   auto slot = [&](int w) -> float* {
-    return (float*)(w == 0 ? sK0 : (w == 1 ? sK1 : (w == 2 ? sV0 : sV1)));
+    char* base = w < 2 ? sK0 : (w < 4 ? sK1 : (w < 6 ? sV0 : sV1));
+    return (float*)(base + (w & 1) * (NJH * 64 * 4));
   };
   float* mine = slot(wave);
-  const float* theirs = slot(wave ^ 2);
-  constexpr int NJ = T::NJ;
-  auto give = [&](auto qo) {
-    constexpr int QO = decltype(qo)::value;
+  const float* theirs = slot(wave ^ 4);
+  auto give = [&](auto half) {
+    constexpr int HF = decltype(half)::value;  // d-half handed to the partner
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) mine[j * 64 + lane] = o[QO][j >> 4][j & 15];
-    sML[(wave * 2 + 0) * 64 + lane] = m[QO];
-    sML[(wave * 2 + 1) * 64 + lane] = lsum[QO];
+    for (int j = 0; j < NJH; ++j) mine[j * 64 + lane] = o[HF * DBH + (j >> 4)][j & 15];
   };
   if (kp) give(IC<0>{}); else give(IC<1>{});
+  sML[(wave * 2 + 0) * 64 + lane] = m;
+  sML[(wave * 2 + 1) * 64 + lane] = lsum;
   __syncthreads();
-  auto finish = [&](auto qf_) {
-    constexpr int QF = decltype(qf_)::value;
+  auto finish = [&](auto half) {
+    constexpr int HF = decltype(half)::value;  // d-half finalised here
     // seed rows: the live diagonal term, one more element of the row's softmax
     const float td = qd_seed ? s_live * c2 : -INFINITY;
-    const float ma = m[QF], la = lsum[QF];
-    const float mb = sML[((wave ^ 2) * 2 + 0) * 64 + lane], lb = sML[((wave ^ 2) * 2 + 1) * 64 + lane];
-    const float mm = fmax3(ma, mb, td);
-    const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
+    const float mb = sML[((wave ^ 4) * 2 + 0) * 64 + lane], lb = sML[((wave ^ 4) * 2 + 1) * 64 + lane];
+    const float mm = fmax3(m, mb, td);
+    const float fa = __builtin_amdgcn_exp2f(m - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
     const float fd = __builtin_amdgcn_exp2f(td - mm);
-    const float ltot = la * fa + lb * fb + fd;
+    const float ltot = lsum * fa + lb * fb + fd;
     const float inv = 1.0f / ltot;
-    const int qf = qd0 + l32;
+    const int qf = qw + l32;
     if (qf < L) {
       __bf16* orow = p.out + b * p.q_sb + h * p.q_sh + (int64_t)qf * p.q_sl;
 #pragma unroll
-      for (int db = 0; db < T::DB; ++db) {
+      for (int dbh = 0; dbh < DBH; ++dbh) {
+        const int db = HF * DBH + dbh;
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int d0 = db * 32 + g4 * 8 + hl * 4;
           f32x4 v;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int j = db * 16 + g4 * 4 + e;
-            v[e] = o[QF][db][g4 * 4 + e] * fa + theirs[j * 64 + lane] * fb;
+            const int j = dbh * 16 + g4 * 4 + e;
+            v[e] = o[db][g4 * 4 + e] * fa + theirs[j * 64 + lane] * fb;
           }
-          if (wave_diag) {
+          if (block_seeded) {
             typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
             const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
                 dg + l32 * T::ROW + ((((d0 >> 3) ^ k_swz<T::ROW>(l32))) << 4) + (d0 & 7) * 2);
@@ -660,7 +576,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
           *(bf16x4*)(orow + d0) = __builtin_convertvector(v, bf16x4);
         }
       }
-      if (p.lse && hl == 0)
+      if (p.lse && hl == 0 && kp == 0)
         p.lse[((int64_t)b * p.Hq + h) * L + qf] = (mm + __builtin_amdgcn_logf(ltot)) * kLn2;
     }
   };
