@@ -164,24 +164,16 @@ __global__ __launch_bounds__(kMaxThreads) void cover_select_kernel(const SelPara
 
 // ---------------------------------------------------------------------------------------
 // Single-wave variant for regions of up to 1024 positions (the paper's generation lengths
-// are 256 and 512): no barriers and no LDS.  Lane l holds positions l + 64 m.  The tree,
-// the counts and the ordering are the same operations as above, so the results are the
-// same bits.
+// are 256 and 512): no barriers and no LDS.  Lane l holds positions l + 64 m, m < E.  The
+// tree, the counts and the ordering are the same operations as above, so the results are
+// the same bits.  E is a template argument so that every per-lane loop is fully unrolled
+// to its real length, and all global loads are issued before the first one is consumed
+// (the kernel is latency bound: one wave, a few hundred positions).
 // ---------------------------------------------------------------------------------------
 constexpr int kWaveMaxPer = 16;  // 64 lanes x 16 = 1024 positions
 
 // DPP full-wave reductions (result valid in lane 63): quad xor 1 and 2, half-row and row
 // mirrors, then row broadcasts 15 and 31.
-template <class F>
-__device__ __forceinline__ int wave_reduce_i32(int x, F op) {
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));  // row_bcast:15
-  x = op(x, __builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));  // row_bcast:31
-  return x;
-}
 template <int CTRL, int RMASK>
 __device__ __forceinline__ double dpp_f64(double x) {
   const uint64_t u = __builtin_bit_cast(uint64_t, x);
@@ -205,81 +197,116 @@ __device__ __forceinline__ double lane63_f64(double x) {
   const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
+__device__ __forceinline__ double first_lane_f64(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((int)(uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((int)(uint32_t)(u >> 32));
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
 
+template <int E>
 __global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p) {
   const int b = blockIdx.x, lane = threadIdx.x;
   const int64_t base = (int64_t)b * p.Lr;
-  const int E = p.per;  // positions per lane (P / 64, at least 1)
-  double sc[kWaveMaxPer];
+
+  // 1. loads: every lane loads all of its E positions (clamped into the row, masked below)
+  //    before any value is used, so the wave waits for one memory round trip, not E.
+  //    An empty region (Lr == 0, input pointers may be null) loads nothing.
+  uint32_t f[E] = {};
+  float lp[E] = {}, di[E] = {}, dq[E] = {};
+  if (p.Lr > 0) {
+#pragma unroll
+    for (int m = 0; m < E; ++m) {
+      const int j = min(lane + 64 * m, p.Lr - 1);
+      f[m] = p.flags[base + j];
+      lp[m] = p.logp[base + j];
+      di[m] = p.d_in[base + j];
+      dq[m] = p.d_out[base + j];
+    }
+  }
+  // 2. scores on U_t, and the masks of U_t and of the eligible positions
+  double sc[E];
   uint32_t umask = 0, emask = 0;
 #pragma unroll
-  for (int m = 0; m < kWaveMaxPer; ++m) {
-    sc[m] = 0.0;
-    const int j = lane + 64 * m;
-    if (m < E && j < p.Lr) {
-      const uint8_t f = p.flags[base + j];
-      const float lp = p.logp[base + j], di = p.d_in[base + j], dq = p.d_out[base + j];
-      if (f & 1u) {
-        const double u = -(double)lp;
-        const double num = u * (1.0 + (double)di);
-        sc[m] = num / (1.0 + (double)dq);
-        umask |= 1u << m;
-        if (!(f & 2u)) emask |= 1u << m;
-      }
-      if (p.score) p.score[base + j] = sc[m];
-    }
+  for (int m = 0; m < E; ++m) {
+    const bool in = lane + 64 * m < p.Lr;
+    const bool u = in && (f[m] & 1u);
+    const double num = -(double)lp[m] * (1.0 + (double)di[m]);
+    const double s = num / (1.0 + (double)dq[m]);
+    sc[m] = u ? s : 0.0;
+    umask |= (uint32_t)u << m;
+    emask |= (uint32_t)(u && !(f[m] & 2u)) << m;
+  }
+  if (p.score) {
+#pragma unroll
+    for (int m = 0; m < E; ++m)
+      if (lane + 64 * m < p.Lr) p.score[base + lane + 64 * m] = sc[m];
   }
   int n = 0, n_elig = 0;
 #pragma unroll
-  for (int m = 0; m < kWaveMaxPer; ++m) {
+  for (int m = 0; m < E; ++m) {
     n += __builtin_popcountll(__builtin_amdgcn_ballot_w64((umask >> m) & 1u));
     n_elig += __builtin_popcountll(__builtin_amdgcn_ballot_w64((emask >> m) & 1u));
   }
-  // canonical tree over P = 64 E (or P < 64) positions: strides >= 64 stay in-lane
-  double a[kWaveMaxPer];
+  // 3. canonical tree over P positions: strides of 64 and more stay inside a lane (position
+  //    lane + 64 m pairs with lane + 64 (m + half)), the last six halvings cross lanes.
+  double a[E];
 #pragma unroll
-  for (int m = 0; m < kWaveMaxPer; ++m) a[m] = sc[m];
+  for (int m = 0; m < E; ++m) a[m] = sc[m];
 #pragma unroll
-  for (int half = kWaveMaxPer / 2; half >= 1; half >>= 1)
-    if (half < E)
+  for (int half = E / 2; half >= 1; half >>= 1)
 #pragma unroll
-      for (int m = 0; m < half; ++m) a[m] = a[m] + a[m + half];
+    for (int m = 0; m < half; ++m) a[m] = a[m] + a[m + half];
   double acc = a[0];
   for (int stride = (p.P < 64 ? p.P : 64) >> 1; stride >= 1; stride >>= 1) {
     const double o = __shfl_down(acc, stride);
     acc = acc + o;  // lanes >= stride compute values that are never used
   }
-  const uint64_t tb = __builtin_bit_cast(uint64_t, acc);
-  const double total = __builtin_bit_cast(double, ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(tb >> 32)) << 32) |
-                                                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)tb));
+  const double total = first_lane_f64(acc);
+  // 4. budget: c = #{ s_j > mean } over U_t, k = ceil(sqrt(c)), clamped
   int c = 0;
   if (n > 0) {
     const double mean = total / (double)n;
 #pragma unroll
-    for (int m = 0; m < kWaveMaxPer; ++m)
+    for (int m = 0; m < E; ++m)
       c += __builtin_popcountll(__builtin_amdgcn_ballot_w64(((umask >> m) & 1u) && sc[m] > mean));
   }
   int k = ceil_isqrt(c);
   k = min(k, n_elig);
   k = min(k, p.max_seeds);
 
-  int mine = 0x7fffffff;  // lane t keeps the t-th winner
-  for (int t = 0; t < k; ++t) {
-    double bs = -1.0;
-    int bj = -1;
+  // 5. top-k by (score desc, position asc).  Each lane keeps its own best remaining slot bm
+  //    (the smallest m among equal scores, i.e. the smallest position); per round the wave
+  //    takes the largest score, then the smallest (m, lane) holding it, and only the winning
+  //    lane rescans.
+  double bs = 0.0;
+  int bm = -1;
+  auto rescan = [&]() {
+    bm = -1;
 #pragma unroll
-    for (int m = 0; m < kWaveMaxPer; ++m) {
-      if ((emask >> m) & 1u) {
-        const int j = lane + 64 * m;
-        if (better(sc[m], j, bs, bj)) { bs = sc[m]; bj = j; }
+    for (int m = 0; m < E; ++m)
+      if (((emask >> m) & 1u) && (bm < 0 || sc[m] > bs)) { bs = sc[m]; bm = m; }
+  };
+  rescan();
+  int mine = 0x7fffffff;  // lane t keeps the t-th winner (k <= 32 < 64)
+  for (int t = 0; t < k; ++t) {
+    const double gmax = lane63_f64(wave_max_f64(bm >= 0 ? bs : -INFINITY));
+    const bool cand = bm >= 0 && bs == gmax;
+    int wm = 0;
+    uint64_t wmask = 0;
+#pragma unroll
+    for (int m = 0; m < E; ++m) {
+      if (wmask == 0) {
+        wmask = __builtin_amdgcn_ballot_w64(cand && bm == m);
+        wm = m;
       }
     }
-    // best score over the wave, then the smallest position holding it
-    const double gmax = lane63_f64(wave_max_f64(bj >= 0 ? bs : -INFINITY));
-    const int cand = (bj >= 0 && bs == gmax) ? bj : 0x7fffffff;
-    const int w = __builtin_amdgcn_readlane(wave_reduce_i32(cand, [](int x, int y) { return x < y ? x : y; }), 63);
-    if ((w & 63) == lane) emask &= ~(1u << (w >> 6));
-    if (lane == t) mine = w;
+    const int wl = (int)__builtin_ctzll(wmask);
+    if (lane == wl) {
+      emask &= ~(1u << wm);
+      rescan();
+    }
+    if (lane == t) mine = wl + 64 * wm;
   }
   int32_t* out = p.seed_idx + (int64_t)b * p.max_seeds;
   if (lane < k) {
@@ -310,7 +337,14 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   p.P = P;
   if (P <= 64 * kWaveMaxPer) {
     p.per = P > 64 ? P / 64 : 1;
-    hipLaunchKernelGGL(cover_select_wave_kernel, dim3((unsigned)a.B), dim3(64), 0, stream, p);
+    const dim3 grid((unsigned)a.B), block(64);
+    switch (p.per) {
+      case 1: hipLaunchKernelGGL(cover_select_wave_kernel<1>, grid, block, 0, stream, p); break;
+      case 2: hipLaunchKernelGGL(cover_select_wave_kernel<2>, grid, block, 0, stream, p); break;
+      case 4: hipLaunchKernelGGL(cover_select_wave_kernel<4>, grid, block, 0, stream, p); break;
+      case 8: hipLaunchKernelGGL(cover_select_wave_kernel<8>, grid, block, 0, stream, p); break;
+      default: hipLaunchKernelGGL(cover_select_wave_kernel<16>, grid, block, 0, stream, p); break;
+    }
     return hipGetLastError();
   }
   int nth = P < 64 ? 64 : (P > kMaxThreads ? kMaxThreads : P);

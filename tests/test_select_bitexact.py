@@ -95,3 +95,30 @@ def test_no_score_buffer_same_selection():
     s = synth.select_inputs(4, 300, seed=3)
     _both(s["logp"].numpy(), s["d_in"].numpy(), s["d_out"].numpy(), s["flags"].numpy(), 20, 0,
           want_score=False)
+
+
+def test_empty_region_on_gpu():
+    announce("select empty region Lr0")
+    B, ms = 3, 5
+    e = torch.empty((B, 0), device="cuda")
+    si, ns, _ = cover.cover_select_seeds(e, e.clone(), e.clone(),
+                                         torch.empty((B, 0), device="cuda", dtype=torch.uint8),
+                                         ms, 0, want_score=False)
+    torch.cuda.synchronize()
+    assert ns.cpu().tolist() == [0] * B
+    assert (si.cpu() == -1).all()
+
+
+@pytest.mark.parametrize("Lr", [64, 256, 1000])
+def test_signed_zero_ties(Lr):
+    """logp of +0.0 gives the score -0.0 and logp of -0.0 gives +0.0: the two compare equal, so
+    the position decides between them; the emitted score keeps its sign bit."""
+    announce(f"select signed-zero ties Lr{Lr}")
+    rng = np.random.default_rng(11 + Lr)
+    B = 16
+    logp = rng.choice(np.array([0.0, -0.0, -0.5, -2.0], np.float32), (B, Lr))
+    d_in = rng.choice(np.array([0.0, 0.25], np.float32), (B, Lr))
+    d_out = np.zeros((B, Lr), np.float32)
+    flags = rng.choice([1, 1, 1, 3], (B, Lr)).astype(np.uint8)
+    for ms in (4, 32):
+        _both(logp, d_in, d_out, flags, ms, 0)
