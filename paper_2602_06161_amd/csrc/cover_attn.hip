@@ -15,19 +15,25 @@
 // removed from the P fed to the main PV product and multiplied by the live value row
 // instead.
 //
-// bf16 kernel design (one workgroup = 4 waves = 128 queries of one (b, h)):
+// bf16 kernel design (one workgroup = 8 waves, two per SIMD = 128 queries of one (b, h)):
 //   * Transposed products keep every query row inside one lane pair:
 //       S^T = K Q^T   (v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q from registers)
 //       O^T += V^T P^T (A = V^T read with ds_read_b64_tr_b16, B = P straight from the S^T
 //                       registers after exp2 and bf16 packing)
 //     so row max / row sum / rescale are lane-local plus one v_permlane32_swap.
-//   * Wave w owns 64 queries (two 32-query blocks, half (w & 1) of the tile) and the keys
-//     of parity (w >> 1): K/V operands read from LDS feed two MFMAs each, halving LDS
-//     traffic relative to 32 queries per wave; the two key halves are merged at the end.
-//   * K/V stages of 64 keys are double buffered in LDS; each row's source (live or cache)
-//     is chosen while loading from a per-sequence seed bitmap in LDS.
+//   * Wave w owns the 32 queries of block w%4 and the 32-key half w/4 of every 64-key
+//     stage; the two key halves of a query block are merged through LDS at the end.  With
+//     256 registers per wave (two waves per SIMD) every MFMA keeps its accumulator in
+//     VGPRs, so the softmax reads S without copies.
+//   * K/V stages of 64 keys: each wave loads an eighth of a stage into registers one step
+//     ahead and stores it to LDS (double-buffered), choosing each row's source (live or
+//     cache) from a per-sequence seed bitmap in LDS; the first stages are loaded from the
+//     live tensors before the bitmap is known and reloaded only if they hold seeds.
+//   * Stages are walked in order; S of the next stage is computed while the softmax and the
+//     PV product of the current one run, with one barrier per stage.
 //   * Lazy softmax rescaling: a row's reference max moves only when the row max grows by
-//     more than 2^8, so most tiles skip the O rescale (exact: O and l share the reference).
+//     more than 2^20, so most stages skip the O rescale (exact: O and l share the
+//     reference).
 //   * Workgroups sharing one (b, key/value head) are placed on the same XCD so its K/V
 //     stays resident in that XCD's L2.
 #include <hip/hip_runtime.h>
@@ -92,17 +98,19 @@ struct Params {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
-// LDS swizzles.  K rows are read 16 rows per LDS cycle at one logical chunk (b128 reads), so
-// the chunk index is XOR-ed with the row (D = 128) or with row/2 (D = 64, two rows per
-// 256-byte bank window).  V rows are read by transpose reads, 4 rows x 2 chunks per 16-lane
-// group, spread by XOR-ing with 2*(row%4).
+// LDS swizzles (64 banks of 4 bytes: one 256-byte window per cycle).  K rows are read 16
+// rows per LDS cycle at one logical chunk (b128 reads), so the chunk index is XOR-ed with
+// the row (D = 128) or with row/2 (D = 64, two rows per 256-byte window).  A V transpose
+// read covers 8 rows x 64 bytes (one 32-column block); the chunk XOR (4*(r%4) for D = 128,
+// 2*(r%4) for D = 64) places the rows' segments so that the 512 bytes fill every bank
+// exactly twice.
 template <int ROW>
 __device__ __forceinline__ int k_swz(int row) {
   return (ROW == 256) ? (row & 15) : ((row >> 1) & 7);
 }
 template <int ROW>
 __device__ __forceinline__ int v_swz(int row) {
-  return (row & 3) << 1;
+  return (ROW == 256) ? ((row & 3) << 2) : ((row & 3) << 1);
 }
 template <int ROW>
 __device__ __forceinline__ uint32_t k_off(int row, int c) {
@@ -189,10 +197,60 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     for (int ks = 0; ks < T::KS; ++ks) qreg[ks] = *(const bf16x8*)(qrow + ks * 16);
   }
 
+  // ---- stage loads -------------------------------------------------------------------------
+  // A stage is 64 rows; each wave moves IPW KiB of it, 16 bytes per lane per KiB, through
+  // registers: load j of this wave holds row (wave*IPW + j)*RPI + lane/CH, physical chunk
+  // lane%CH, which is the row's logical chunk (physical ^ swizzle), and is stored to LDS at
+  // (wave*IPW + j)*1024 + 16*lane.  A row comes from the cache when its position is a seed;
+  // rows past L (ragged last stage) repeat row L-1 (their scores are masked).
+  auto ld_row = [&](int j) { return (wave * T::IPW + j) * T::RPI + lane / T::CH; };
+  auto ld_chunk = [&](int j, bool is_v) -> uint32_t {
+    const int row = ld_row(j), pc = lane % T::CH;
+    return (uint32_t)((pc ^ (is_v ? (v_swz<T::ROW>(row) & (T::CH - 1)) : k_swz<T::ROW>(row))) << 4);
+  };
+  const int64_t row_bytes = p.kv_sl * 2;
+  const int64_t stage_bytes = kStageKeys * row_bytes;
+  uint32_t offK[T::IPW], offV[T::IPW];
+#pragma unroll
+  for (int j = 0; j < T::IPW; ++j) {
+    offK[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, false);
+    offV[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, true);
+  }
+  auto uniform_ptr = [](const void* ptr) -> gmem_t* {
+    const uint64_t v = (uint64_t)ptr;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (gmem_t*)(((uint64_t)hi << 32) | lo);
+  };
+  gmem_t* const klb = uniform_ptr(p.kl + kvoff);
+  gmem_t* const kcb = uniform_ptr(p.kc + kvoff);
+  gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
+  gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
+  typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+
+  // The first stages are loaded speculatively from the live tensors (rows past L clamped),
+  // in the shadow of the seed list's latency; stages that turn out to hold seeds are loaded
+  // again once the bitmap is known.  K(0), V(0), K(1) go to pre[], K(2), V(1) to staging.
+  const int n_it = (L + kStageKeys - 1) / kStageKeys;
+  auto clamp_stage = [=](int i) -> int { return i < n_it ? i : n_it - 1; };
+  auto ld_live = [&](u32x4* st, gmem_t* live, bool is_v, int stage) {
+    const int kb = stage * kStageKeys;
+#pragma unroll
+    for (int j = 0; j < T::IPW; ++j) {
+      const int key = min(kb + ld_row(j), L - 1);
+      st[j] = *(gu32x4*)(live + key * row_bytes + ld_chunk(j, is_v));
+    }
+  };
+  u32x4 pre[3][T::IPW], stgK[T::IPW], stgV[T::IPW];
+  ld_live(pre[0], klb, false, 0);
+  ld_live(pre[1], vlb, true, 0);
+  ld_live(pre[2], klb, false, clamp_stage(1));
+  ld_live(stgK, klb, false, clamp_stage(2));
+  ld_live(stgV, vlb, true, clamp_stage(1));
+
   // ---- seed bitmap of this sequence ---------------------------------------------------
   // The seed list is read speculatively (the first kThreads entries) with its length.
   const int nwords = (L + 31) >> 5;
-  const int n_it = (L + kStageKeys - 1) / kStageKeys;
   const int64_t sbase = (int64_t)b * p.max_seeds;
   int ns = 0;
   if (p.max_seeds > 0) ns = p.n_seed[b];
@@ -234,38 +292,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
                                           : __builtin_amdgcn_readlane(dirty_lo, stage >> 6);
     return (w >> (stage & 31)) & 1u;
   };
-  auto clamp_stage = [=](int i) -> int { return i < n_it ? i : n_it - 1; };
 
-  // ---- stage loads -------------------------------------------------------------------------
-  // A stage is 64 rows; each wave moves IPW KiB of it, 16 bytes per lane per KiB, through
-  // registers: load j of this wave holds row (wave*IPW + j)*RPI + lane/CH, physical chunk
-  // lane%CH, which is the row's logical chunk (physical ^ swizzle), and is stored to LDS at
-  // (wave*IPW + j)*1024 + 16*lane.  A row comes from the cache when its position is a seed;
-  // rows past L (ragged last stage) repeat row L-1 (their scores are masked).
-  auto ld_row = [&](int j) { return (wave * T::IPW + j) * T::RPI + lane / T::CH; };
-  auto ld_chunk = [&](int j, bool is_v) -> uint32_t {
-    const int row = ld_row(j), pc = lane % T::CH;
-    return (uint32_t)((pc ^ (is_v ? (v_swz<T::ROW>(row) & (T::CH - 1)) : k_swz<T::ROW>(row))) << 4);
-  };
-  const int64_t row_bytes = p.kv_sl * 2;
-  const int64_t stage_bytes = kStageKeys * row_bytes;
-  uint32_t offK[T::IPW], offV[T::IPW];
-#pragma unroll
-  for (int j = 0; j < T::IPW; ++j) {
-    offK[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, false);
-    offV[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, true);
-  }
-  auto uniform_ptr = [](const void* ptr) -> gmem_t* {
-    const uint64_t v = (uint64_t)ptr;
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    return (gmem_t*)(((uint64_t)hi << 32) | lo);
-  };
-  gmem_t* const klb = uniform_ptr(p.kl + kvoff);
-  gmem_t* const kcb = uniform_ptr(p.kc + kvoff);
-  gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
-  gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
-  typedef __attribute__((address_space(1))) const u32x4 gu32x4;
   // Issue the loads of one stage of K or V into st[0..IPW).  Stages without seeds and within
   // L use a scalar base and per-lane 32-bit offsets; the others choose each row's source and
   // clamp rows past L.
@@ -377,11 +404,12 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
       for (int r = 0; r < 16; ++r) s[r] = (diag_seed && r == rd) ? -INFINITY : s[r];
     }
   };
+  // a tree of depth 3 (independent max3 operations first), not a chain of 8
   auto lane_max = [&](const f32x16& s) -> float {
-    float x = fmax3(s[0], s[1], s[2]);
-#pragma unroll
-    for (int r = 3; r < 15; r += 2) x = fmax3(x, s[r], s[r + 1]);
-    return fmax2(x, s[15]);
+    const float a = fmax3(s[0], s[1], s[2]), b = fmax3(s[3], s[4], s[5]);
+    const float c = fmax3(s[6], s[7], s[8]), d = fmax3(s[9], s[10], s[11]);
+    const float e = fmax3(s[12], s[13], s[14]);
+    return fmax3(fmax3(a, b, c), fmax2(d, e), s[15]);
   };
 
   float m, lsum = 0.0f, thr;
@@ -403,16 +431,17 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     bf16x8 pk[2];
     pk[0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
     pk[1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
-    float ls = lsum;
+    // row sums in two independent chains of four
+    float ls[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const bf16x8 w = pk[kk];
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, ls, false);
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, ls, false);
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, ls, false);
-      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, ls, false);
+      float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, 0.0f, false);
+      a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, a, false);
+      a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, a, false);
+      ls[kk] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, a, false);
     }
-    lsum = ls;
+    lsum += ls[0] + ls[1];
     typedef short i16x8 __attribute__((ext_vector_type(8)));
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -427,15 +456,17 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
 
   // ---- prologue ------------------------------------------------------------------------------
   // K(0), V(0), K(1) go straight to their buffers; K(2) and V(1) wait in the staging
-  // registers for the first step.  Then S(0) and the reference row max.
-  u32x4 stgK[T::IPW], stgV[T::IPW];
+  // registers for the first step (all loaded before the bitmap, again here if they hold
+  // seeds).  Then S(0) and the reference row max.
   {
-    u32x4 pre[3][T::IPW];
-    ld(pre[0], klb, kcb, offK, false, 0);
-    ld(pre[1], vlb, vcb, offV, true, 0);
-    ld(pre[2], klb, kcb, offK, false, clamp_stage(1));
-    ld(stgK, klb, kcb, offK, false, clamp_stage(2));
-    ld(stgV, vlb, vcb, offV, true, clamp_stage(1));
+    if (dirty(0) || dirty(clamp_stage(1)) || dirty(clamp_stage(2))) {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // the speculative loads are replaced
+      ld(pre[0], klb, kcb, offK, false, 0);
+      ld(pre[1], vlb, vcb, offV, true, 0);
+      ld(pre[2], klb, kcb, offK, false, clamp_stage(1));
+      ld(stgK, klb, kcb, offK, false, clamp_stage(2));
+      ld(stgV, vlb, vcb, offV, true, clamp_stage(1));
+    }
     __builtin_amdgcn_s_waitcnt(T::kWaitPrev);  // the first three stages landed
     st(pre[0], kbuf(0));
     st(pre[1], vbuf(0));
@@ -531,7 +562,11 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   auto give = [&](auto half) {
     constexpr int HF = decltype(half)::value;  // d-half handed to the partner
 #pragma unroll
-    for (int j = 0; j < NJH; ++j) mine[j * 64 + lane] = o[HF * DBH + (j >> 4)][j & 15];
+    for (int j = 0; j < NJH; j += 4) {
+      const f32x16& src = o[HF * DBH + (j >> 4)];
+      const f32x4 v = {src[(j & 15) + 0], src[(j & 15) + 1], src[(j & 15) + 2], src[(j & 15) + 3]};
+      *(f32x4*)(mine + (j >> 2) * 256 + lane * 4) = v;  // four values of a lane are contiguous
+    }
   };
   if (kp) give(IC<0>{}); else give(IC<1>{});
   sML[(wave * 2 + 0) * 64 + lane] = m;
@@ -556,12 +591,10 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int d0 = db * 32 + g4 * 8 + hl * 4;
+          const f32x4 tv = *(const f32x4*)(theirs + (dbh * 4 + g4) * 256 + lane * 4);
           f32x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int j = dbh * 16 + g4 * 4 + e;
-            v[e] = o[db][g4 * 4 + e] * fa + theirs[j * 64 + lane] * fb;
-          }
+          for (int e = 0; e < 4; ++e) v[e] = o[db][g4 * 4 + e] * fa + tv[e] * fb;
           if (block_seeded) {
             typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
             const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
