@@ -13,6 +13,10 @@ on seeded synthetic inputs already resident in HBM.  Prints one JSON line.
 Profiling helpers (what the committed rocprofv3 summaries were made with):
   --only attn|select   time only that kernel in the step
   --copy-mib N         run a plain device copy of N MiB (HBM counter calibration)
+  --kernel token_stats|attn_stats
+                       time one producer of the selection inputs at the LLaDA-8B step shape
+                       (the LM head's 256 x 126464 bf16 logits; the 256-position generated
+                       block of the last layer) and print its own JSON line
 """
 from __future__ import annotations
 
@@ -65,6 +69,7 @@ def main() -> int:
     ap.add_argument("--only", choices=["attn", "select"], default=None)
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel", choices=["token_stats", "attn_stats"], default=None)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -90,6 +95,9 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_mib": args.copy_mib, "launches": args.steps}))
         return 0
+
+    if args.kernel:
+        return bench_producer(args, dev, stream)
 
     a = synth.step_inputs(args.workload, seed=args.seed)
     c = a["cfg"]
@@ -196,6 +204,73 @@ def main() -> int:
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(a, flops)
     print(json.dumps(rec))
+    return 0
+
+
+def bench_producer(args, dev, stream) -> int:
+    """One producer of the selection signals, K back-to-back launches between two events."""
+    import ctypes
+
+    import torch
+    from paper_2602_06161_amd import cover, synth
+
+    if args.kernel == "token_stats":
+        R, V = 256, 126464
+        t = synth.token_inputs(R, V, seed=args.seed)
+        logits = t["buffer"].to(dev)[:, :V]
+        tokens = t["tokens"].to(dev)
+        outs = [torch.empty(R, device=dev, dtype=dt) for dt in (torch.float32, torch.float32,
+                                                                 torch.int32)]
+        desc = cover.TokenDesc(R, V, cover.COVER_BF16, logits.stride(0))
+        cargs = [cover._ptr(logits), cover._ptr(tokens)] + [cover._ptr(o) for o in outs] + \
+                [ctypes.byref(desc), cover._stream(stream)]
+        fn = cover.lib().cover_token_stats
+        run = lambda: fn(*cargs)  # arguments marshalled once (no Python work per launch)
+        nbytes = R * V * 2 + R * 16  # logits once; token id in; logp, conf, argmax out
+        cfg = {"workload": f"LLaDA-8B LM-head block: R={R} positions x V={V} bf16 logits"}
+        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+    else:
+        a = synth.stats_inputs("llada", seed=args.seed)
+        t = {k: a[k].to(dev) for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx",
+                                         "n_seed", "masked", "drafted")}
+        _, lse = cover.cover_attn_fwd(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
+                                      t["seed_idx"], t["n_seed"], stream=stream)
+        c = a["cfg"]
+        ws = torch.empty(cover.attn_stats_workspace(c.B, c.Hq, a["Lr"]), device=dev,
+                         dtype=torch.float32)
+        d_in = torch.empty((c.B, a["Lr"]), device=dev, dtype=torch.float32)
+        d_out = torch.empty_like(d_in)
+        desc = cover.StatsDesc(cover.attn_desc(t["q"], t["k_live"], t["seed_idx"].shape[-1]),
+                               a["r0"], a["Lr"])
+        cargs = [cover._ptr(x) for x in (t["q"], t["k_live"], t["k_cache"], t["seed_idx"],
+                                         t["n_seed"], lse, t["masked"], t["drafted"], d_in, d_out,
+                                         ws)] + [ctypes.byref(desc), cover._stream(stream)]
+        fn = cover.lib().cover_attn_stats
+        run = lambda: fn(*cargs)
+        nbytes = None
+        flops = 2 * c.B * c.Hq * a["Lr"] * a["Lr"] * c.d  # one QK^T over the region
+        cfg = {"workload": f"LLaDA-8B last layer, generated block: B={c.B} Hq={c.Hq} "
+                           f"Lr={a['Lr']} of L={c.L}, d={c.d} bf16"}
+        bound, unit, peak = "latency", "TFLOP/s", PEAK_BF16_TFLOPS
+    for _ in range(args.warmup):
+        if run() != 0:
+            raise RuntimeError(f"{args.kernel} launch rejected")
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / args.steps
+    if nbytes is not None:
+        achieved = nbytes / (us * 1e-6) / 1e9
+    else:
+        achieved = flops / (us * 1e-6) / 1e12
+    print(json.dumps({"kernel": args.kernel, "us_per_launch": round(us, 3), "steps": args.steps,
+                      "config": cfg, "roofline": {"bound": bound, "achieved": round(achieved, 2),
+                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
+                      "algorithmic_bytes_per_launch": nbytes}}))
     return 0
 
 

@@ -9,6 +9,11 @@
  *                       diagonal correction for seed rows (Sec. 5.1; App. B).
  *   cover_select_seeds  stability-aware seed scoring, adaptive budget and top-k
  *                       (Sec. 5.3).
+ * and the producers of the selection's inputs:
+ *   cover_token_stats   log p of the current token, confidence and argmax per position
+ *                       (Sec. 5.3 u(j); Sec. 3 confidence and draft token).
+ *   cover_attn_stats    in/out attention masses d_in, d_out over the response region
+ *                       (Sec. 5.3 signals).
  *
  * Conventions shared by every entry point
  *   - Every data pointer is device memory owned by the caller (hipMalloc, or a framework
@@ -151,6 +156,79 @@ cover_status cover_select_seeds(const float* logp, const float* d_in, const floa
                                 const uint8_t* flags,
                                 int32_t* seed_idx, int32_t* n_seed, double* score,
                                 const cover_select_desc* desc, hipStream_t stream);
+
+/*
+ * Token statistics description.
+ *   R           rows (positions; >= 0, 0 is a no-op)
+ *   V           vocabulary size (>= 1)
+ *   dtype       element type of logits (COVER_BF16 or COVER_F32)
+ *   row_stride  elements between consecutive rows of logits (>= V); the base pointer and
+ *               row_stride * element size must be multiples of 16 bytes
+ */
+typedef struct {
+  int32_t R, V;
+  cover_dtype dtype;
+  int64_t row_stride;
+} cover_token_desc;
+
+/*
+ * cover_token_stats -- per-position statistics of the model's output distribution
+ * (Sec. 5.3: u(j) = -log p_j(y_j); Sec. 3: confidence = max_v p_j(v), draft token = argmax).
+ *
+ * For row r with logits x_r[0..V) and lz_r = log sum_v exp(x_r[v]) (natural log):
+ *   logp[r]   = x_r[tokens[r]] - lz_r
+ *   conf[r]   = exp(max_v x_r[v] - lz_r)
+ *   argmax[r] = the smallest v attaining max_v x_r[v]
+ * Arithmetic in fp32 (exp/log of the exp2/log2 units); one pass over the logits.
+ * Arguments: logits [R, row_stride] (device); tokens int32 [R] (device; may be NULL when
+ * logp is NULL); logp, conf fp32 [R] and argmax int32 [R] (device outputs, each may be
+ * NULL).  Device-data contract: tokens in [0, V) (a token outside gives logp = NaN, never
+ * an out-of-bounds read); logits finite.
+ */
+cover_status cover_token_stats(const void* logits, const int32_t* tokens,
+                               float* logp, float* conf, int32_t* argmax,
+                               const cover_token_desc* desc, hipStream_t stream);
+
+/*
+ * Attention-mass description: the attention problem of cover_attn_fwd (same fields and
+ * stride rules; bf16 only) plus the response region [r0, r0 + Lr).
+ *   r0, Lr      0 <= r0, 1 <= Lr, r0 + Lr <= L (Lr == 0 is a no-op)
+ */
+typedef struct {
+  cover_attn_desc attn;
+  int32_t r0, Lr;
+} cover_stats_desc;
+
+/* Largest response region cover_attn_stats accepts. */
+#define COVER_STATS_MAX_LR 2048
+/* Workspace of cover_attn_stats in floats: B * Hq * 2 * Lr. */
+#define COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr) ((int64_t)(B) * (Hq) * 2 * (Lr))
+
+/*
+ * cover_attn_stats -- the in/out attention masses of Sec. 5.3 from the last layer's
+ * corrected attention weights, averaged over query heads, restricted to the response region.
+ *
+ * With w^(h)_{i,j} = exp(scale <q_i, K^(i)_j> - lse[b,h,i]) the weights of cover_attn_fwd
+ * (override memory, leave-one-out view for seed rows, normalised over all L positions by
+ * the lse that call returned) and A_{i->j} = (1/Hq) sum_h w^(h)_{i,j}, for region positions
+ * j = r0 + t, t in [0, Lr):
+ *   d_in[b,t]  = sum over region rows i with masked[b, i-r0]  of A_{i->j}
+ *   d_out[b,t] = sum over region columns i with drafted[b, i-r0] of A_{j->i}
+ * Arguments: q, k_live, k_cache, seed_idx, n_seed as for cover_attn_fwd (v is not needed);
+ * lse fp32 [B,Hq,L] contiguous, as returned by cover_attn_fwd for the same inputs;
+ * masked, drafted uint8 [B,Lr] (nonzero = member; device); d_in, d_out fp32 [B,Lr]
+ * (device outputs); workspace: device fp32 buffer of COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr)
+ * floats owned by the caller (its contents on entry are ignored, on exit unspecified).
+ * Two kernel launches on `stream`; partial sums are added in a fixed order, so the results
+ * are deterministic.  Weights are formed in fp32 from the fp32 lse.
+ * Returns COVER_ERR_UNSUPPORTED for a dtype other than bf16, d not in {64, 128},
+ * L > COVER_MAX_L or Lr > COVER_STATS_MAX_LR.
+ */
+cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
+                              const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
+                              const uint8_t* masked, const uint8_t* drafted,
+                              float* d_in, float* d_out, float* workspace,
+                              const cover_stats_desc* desc, hipStream_t stream);
 
 /* Static string naming a status code. */
 const char* cover_status_str(cover_status s);

@@ -19,7 +19,8 @@ COVER_F32, COVER_BF16 = 0, 1
 COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
 
-EXPORTED = ("cover_attn_fwd", "cover_select_seeds", "cover_status_str", "cover_version")
+EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_select_seeds", "cover_status_str",
+            "cover_token_stats", "cover_version")
 
 
 class CoverError(RuntimeError):
@@ -41,6 +42,20 @@ class SelectDesc(ctypes.Structure):
                 ("pos_offset", ctypes.c_int32)]
 
 
+class TokenDesc(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_int32), ("V", ctypes.c_int32), ("dtype", ctypes.c_int),
+                ("row_stride", ctypes.c_int64)]
+
+
+class StatsDesc(ctypes.Structure):
+    _fields_ = [("attn", AttnDesc), ("r0", ctypes.c_int32), ("Lr", ctypes.c_int32)]
+
+
+def attn_stats_workspace(B: int, Hq: int, Lr: int) -> int:
+    """Floats of workspace cover_attn_stats needs (COVER_ATTN_STATS_WORKSPACE)."""
+    return B * Hq * 2 * Lr
+
+
 _lib = None
 
 
@@ -57,6 +72,10 @@ def lib():
         L.cover_attn_fwd.restype = ctypes.c_int
         L.cover_select_seeds.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(SelectDesc), P]
         L.cover_select_seeds.restype = ctypes.c_int
+        L.cover_token_stats.argtypes = [P, P, P, P, P, ctypes.POINTER(TokenDesc), P]
+        L.cover_token_stats.restype = ctypes.c_int
+        L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
+        L.cover_attn_stats.restype = ctypes.c_int
         L.cover_status_str.argtypes = [ctypes.c_int]
         L.cover_status_str.restype = ctypes.c_char_p
         L.cover_version.argtypes = []
@@ -150,6 +169,61 @@ def cover_select_seeds(logp, d_in, d_out, flags, max_seeds: int, pos_offset: int
     if st != COVER_OK:
         raise CoverError(st, "cover_select_seeds")
     return seed_idx, n_seed, score
+
+
+def cover_token_stats(logits, tokens=None, want_logp: bool = True, want_conf: bool = True,
+                      want_argmax: bool = True, stream=None):
+    """Per-row log p(token), max probability and argmax of logits [R, V] (bf16 or fp32, last
+    dimension contiguous, row stride a multiple of 16 bytes).  Returns (logp, conf, argmax),
+    each None when not requested."""
+    R, V = logits.shape
+    dt = {torch.float32: COVER_F32, torch.bfloat16: COVER_BF16}.get(logits.dtype)
+    if dt is None or logits.stride(-1) != 1:
+        raise ValueError("logits must be bf16 or fp32 with a contiguous last dimension")
+    if want_logp and (tokens is None or tokens.dtype != torch.int32 or tokens.shape != (R,)
+                      or not tokens.is_contiguous()):
+        raise ValueError("tokens must be a contiguous int32 [R] tensor")
+    dev = logits.device
+    logp = torch.empty(R, device=dev, dtype=torch.float32) if want_logp else None
+    conf = torch.empty(R, device=dev, dtype=torch.float32) if want_conf else None
+    amax = torch.empty(R, device=dev, dtype=torch.int32) if want_argmax else None
+    desc = TokenDesc(R, V, dt, logits.stride(0))
+    st = lib().cover_token_stats(_ptr(logits), _ptr(tokens if want_logp else None), _ptr(logp),
+                                 _ptr(conf), _ptr(amax), ctypes.byref(desc), _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_token_stats")
+    return logp, conf, amax
+
+
+def cover_attn_stats(q, k_live, k_cache, seed_idx, n_seed, lse, masked, drafted, r0: int,
+                     scale: float = 0.0, workspace=None, stream=None):
+    """d_in, d_out [B, Lr] over the region [r0, r0+Lr) (Lr = masked.shape[1]) from the corrected
+    attention weights of cover_attn_fwd (lse from that call).  bf16 q/k; masked, drafted
+    uint8 [B, Lr]."""
+    B, Hq, L, d = q.shape
+    Lr = masked.shape[1]
+    for t in (k_live, k_cache):
+        if t.shape != k_live.shape or t.stride() != k_live.stride() or t.dtype != q.dtype:
+            raise ValueError("k_live and k_cache need equal shape, strides and dtype")
+    for t in (masked, drafted):
+        if t.shape != (B, Lr) or t.dtype != torch.uint8 or not t.is_contiguous():
+            raise ValueError("masked / drafted must be contiguous uint8 [B, Lr]")
+    if lse.shape != (B, Hq, L) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be contiguous fp32 [B, Hq, L]")
+    max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+    dev = q.device
+    d_in = torch.empty((B, Lr), device=dev, dtype=torch.float32)
+    d_out = torch.empty((B, Lr), device=dev, dtype=torch.float32)
+    if workspace is None:
+        workspace = torch.empty(max(1, attn_stats_workspace(B, Hq, Lr)), device=dev,
+                                dtype=torch.float32)
+    desc = StatsDesc(attn_desc(q, k_live, max_seeds, scale), int(r0), int(Lr))
+    st = lib().cover_attn_stats(_ptr(q), _ptr(k_live), _ptr(k_cache), _ptr(seed_idx),
+                                _ptr(n_seed), _ptr(lse), _ptr(masked), _ptr(drafted), _ptr(d_in),
+                                _ptr(d_out), _ptr(workspace), ctypes.byref(desc), _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_attn_stats")
+    return d_in, d_out
 
 
 def attn_flops(B: int, Hq: int, L: int, d: int) -> int:

@@ -101,4 +101,68 @@ cover_status cover_select_seeds(const float* logp, const float* d_in, const floa
   return hip_status(cover::launch_select(a, stream));
 }
 
+cover_status cover_token_stats(const void* logits, const int32_t* tokens,
+                               float* logp, float* conf, int32_t* argmax,
+                               const cover_token_desc* desc, hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_token_desc& D = *desc;
+  if (D.R < 0 || D.V < 1 || D.row_stride < D.V) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_F32 && D.dtype != COVER_BF16) return COVER_ERR_INVALID;
+  const int64_t esz = D.dtype == COVER_BF16 ? 2 : 4;
+  if ((D.row_stride * esz) % 16 != 0) return COVER_ERR_INVALID;
+  if (D.R == 0) return COVER_OK;
+  if (!logits || !aligned(logits, 16)) return COVER_ERR_INVALID;
+  if (logp && (!tokens || !aligned(tokens, 4) || !aligned(logp, 4))) return COVER_ERR_INVALID;
+  if ((conf && !aligned(conf, 4)) || (argmax && !aligned(argmax, 4))) return COVER_ERR_INVALID;
+  cover::TokenArgs a;
+  a.logits = logits; a.tokens = tokens; a.logp = logp; a.conf = conf; a.argmax = argmax;
+  a.R = D.R; a.V = D.V; a.bf16 = D.dtype == COVER_BF16; a.row_stride = D.row_stride;
+  return hip_status(cover::launch_token_stats(a, stream));
+}
+
+cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
+                              const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
+                              const uint8_t* masked, const uint8_t* drafted,
+                              float* d_in, float* d_out, float* workspace,
+                              const cover_stats_desc* desc, hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_attn_desc& D = desc->attn;
+  const int32_t r0 = desc->r0, Lr = desc->Lr;
+  if (D.B < 0 || D.L < 0 || D.Hq < 1 || D.Hkv < 1 || D.d < 1 || D.max_seeds < 0)
+    return COVER_ERR_INVALID;
+  if (D.Hq % D.Hkv != 0) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_F32 && D.dtype != COVER_BF16) return COVER_ERR_INVALID;
+  if (!(D.scale >= 0.0f) || isinf(D.scale)) return COVER_ERR_INVALID;
+  if (r0 < 0 || Lr < 0 || (int64_t)r0 + Lr > D.L) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_BF16) return COVER_ERR_UNSUPPORTED;
+  if (D.d != 64 && D.d != 128) return COVER_ERR_UNSUPPORTED;
+  if (D.L > COVER_MAX_L || Lr > COVER_STATS_MAX_LR) return COVER_ERR_UNSUPPORTED;
+  if (D.B == 0 || Lr == 0) return COVER_OK;
+  const void* tensors[3] = {q, k_live, k_cache};
+  for (const void* t : tensors)
+    if (!t || !aligned(t, 16)) return COVER_ERR_INVALID;
+  const int64_t strides[6] = {D.q_sb, D.q_sh, D.q_sl, D.kv_sb, D.kv_sh, D.kv_sl};
+  for (int64_t s : strides)
+    if (s < 0 || s % 8 != 0) return COVER_ERR_INVALID;
+  if (D.L > 1 && (D.q_sl < D.d || D.kv_sl < D.d)) return COVER_ERR_INVALID;
+  if (D.max_seeds > 0 && (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4)))
+    return COVER_ERR_INVALID;
+  if (!lse || !aligned(lse, 4) || !masked || !drafted) return COVER_ERR_INVALID;
+  if (!d_in || !d_out || !workspace || !aligned(d_in, 4) || !aligned(d_out, 4) ||
+      !aligned(workspace, 4))
+    return COVER_ERR_INVALID;
+  cover::StatsArgs a;
+  a.q = q; a.k_live = k_live; a.k_cache = k_cache;
+  a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
+  a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
+  a.lse = lse; a.masked = masked; a.drafted = drafted;
+  a.d_in = d_in; a.d_out = d_out; a.workspace = workspace;
+  a.B = D.B; a.Hq = D.Hq; a.Hkv = D.Hkv; a.L = D.L; a.d = D.d; a.max_seeds = D.max_seeds;
+  a.r0 = r0; a.Lr = Lr;
+  a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
+  a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
+  a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  return hip_status(cover::launch_attn_stats(a, stream));
+}
+
 }  // extern "C"

@@ -32,8 +32,38 @@ struct SelectArgs {
   int32_t B, Lr, max_seeds, pos_offset;
 };
 
+struct TokenArgs {
+  const void* logits;
+  const int32_t* tokens;  // may be null when logp is null
+  float* logp;            // may be null
+  float* conf;            // may be null
+  int32_t* argmax;        // may be null
+  int32_t R, V;
+  int bf16;               // element type of logits: bf16 (1) or fp32 (0)
+  int64_t row_stride;     // elements
+};
+
+struct StatsArgs {
+  const void* q;
+  const void* k_live;
+  const void* k_cache;
+  const int32_t* seed_idx;  // may be null when max_seeds == 0
+  const int32_t* n_seed;    // may be null when max_seeds == 0
+  const float* lse;
+  const uint8_t* masked;
+  const uint8_t* drafted;
+  float* d_in;
+  float* d_out;
+  float* workspace;
+  int32_t B, Hq, Hkv, L, d, max_seeds, r0, Lr;
+  float scale;  // > 0
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
+hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
 
 }  // namespace cover

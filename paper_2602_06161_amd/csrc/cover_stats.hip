@@ -1,0 +1,365 @@
+// Producers of the seed-selection signals on gfx950 (arXiv 2602.06161, Sec. 5.3; Sec. 3).
+//
+// cover_token_stats_kernel: per row of the model's output logits, the log-probability of the
+// token currently placed there (u = -log p, Sec. 5.3), the maximum probability (the
+// confidence of Sec. 3) and the token attaining it.  One workgroup of 1024 threads per row;
+// HBM-bound: each thread streams 16-byte chunks with four loads in flight and keeps an
+// online (max, sum of exp, argmax) triple, merged across the workgroup at the end.
+//
+// cover_attn_stats_kernel + cover_attn_stats_reduce_kernel: the in/out attention masses of
+// Sec. 5.3 over a response region [r0, r0+Lr), from the last layer's corrected weights
+// w_qj = exp(scale q.K^(q)_j - lse_q) (the same leave-one-out rows the attention computes,
+// normalised over the whole sequence by the forward pass's lse), averaged over query heads:
+//   d_in(j)  = (1/Hq) sum_h sum_{q masked} w_qj,    d_out(j) = (1/Hq) sum_h sum_{i drafted} w_ji
+// One workgroup per (batch row, query head); each of its waves takes 32-query blocks of the
+// region and forms both S = Q K^T and S^T = K Q^T tile by tile (the same operand registers,
+// swapped), so each mass is a sum inside a lane.  Per-head masses go to a caller-provided
+// workspace and a second kernel averages them over heads; every sum runs in a fixed order,
+// so the results do not depend on scheduling.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace cover {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+
+constexpr int kTokThreads = 1024;
+constexpr int kTokUnroll = 4;  // 16-byte loads in flight per thread
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kLn2 = 0.693147180559945309f;
+
+struct TokParams {
+  const char* logits;
+  const int32_t* tokens;
+  float* logp;
+  float* conf;
+  int32_t* argmax;
+  int64_t row_stride_bytes;
+  int V;
+  int bf16;
+};
+
+// (m, s, i): running max, sum of exp2((x - m) * log2e) over the elements seen, the smallest
+// index holding m.  Merging two triples keeps the larger max (smaller index on ties).
+struct Acc {
+  float m, s;
+  int i;
+};
+__device__ __forceinline__ Acc merge(Acc a, Acc b) {
+  const float m = fmaxf(a.m, b.m);
+  Acc r;
+  r.m = m;
+  const float sa = a.s == 0.0f ? 0.0f : a.s * __builtin_amdgcn_exp2f((a.m - m) * kLog2e);
+  const float sb = b.s == 0.0f ? 0.0f : b.s * __builtin_amdgcn_exp2f((b.m - m) * kLog2e);
+  r.s = sa + sb;
+  r.i = a.m > b.m ? a.i : (b.m > a.m ? b.i : min(a.i, b.i));
+  return r;
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fold the n (<= 8) values of one chunk, starting at element index j0, into acc
+__device__ __forceinline__ void fold(Acc& acc, const float* x, int n, int j0) {
+  float cm = x[0];
+  int ci = j0;
+#pragma unroll
+  for (int e = 1; e < 8; ++e)
+    if (e < n && x[e] > cm) { cm = x[e]; ci = j0 + e; }
+  if (cm > acc.m) {
+    acc.s = acc.s == 0.0f ? 0.0f : acc.s * __builtin_amdgcn_exp2f((acc.m - cm) * kLog2e);
+    acc.m = cm;
+    acc.i = ci;
+  }
+  const float nm = -acc.m * kLog2e;
+  float add = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (e < n) add += __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], kLog2e, nm));
+  acc.s += add;
+}
+
+__global__ __launch_bounds__(kTokThreads) void cover_token_stats_kernel(const TokParams p) {
+  __shared__ float sm[kTokThreads / 64], ss[kTokThreads / 64];
+  __shared__ int si[kTokThreads / 64];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const char* row = p.logits + (int64_t)r * p.row_stride_bytes;
+  const int per = p.bf16 ? 8 : 4;  // elements per 16-byte chunk
+  const int nfull = p.V / per;      // whole chunks; the last V % per elements come after
+  Acc acc = {-INFINITY, 0.0f, 0x7fffffff};
+  for (int c0 = tid; c0 < nfull; c0 += kTokThreads * kTokUnroll) {
+    u32x4 v[kTokUnroll];
+#pragma unroll
+    for (int u = 0; u < kTokUnroll; ++u) {
+      const int c = c0 + u * kTokThreads;
+      v[u] = c < nfull ? *(gu32x4*)((__attribute__((address_space(1))) const char*)row + (int64_t)c * 16) : (u32x4){};
+    }
+#pragma unroll
+    for (int u = 0; u < kTokUnroll; ++u) {
+      const int c = c0 + u * kTokThreads;
+      if (c >= nfull) break;
+      float x[8];
+      if (p.bf16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { x[2 * e] = bf_lo(v[u][e]); x[2 * e + 1] = bf_hi(v[u][e]); }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(v[u][e]); x[e + 4] = -INFINITY; }
+      }
+      fold(acc, x, per, c * per);
+    }
+  }
+  // the tail: one element per thread, read at its own width (never past the row's end)
+  if (tid < p.V - nfull * per) {
+    const int j = nfull * per + tid;
+    float x[8];
+    x[0] = p.bf16 ? __uint_as_float((uint32_t)(*(const uint16_t*)(row + (int64_t)j * 2)) << 16)
+                  : *(const float*)(row + (int64_t)j * 4);
+    fold(acc, x, 1, j);
+  }
+  // wave, then workgroup
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Acc o;
+    o.m = __shfl_xor(acc.m, off);
+    o.s = __shfl_xor(acc.s, off);
+    o.i = __shfl_xor(acc.i, off);
+    acc = merge(acc, o);
+  }
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; si[wave] = acc.i; }
+  __syncthreads();
+  if (tid == 0) {
+    Acc t = {sm[0], ss[0], si[0]};
+    for (int w = 1; w < kTokThreads / 64; ++w) t = merge(t, Acc{sm[w], ss[w], si[w]});
+    const float lz = t.m + __builtin_amdgcn_logf(t.s) * kLn2;  // natural log-sum-exp
+    if (p.conf) p.conf[r] = 1.0f / t.s;                         // exp(max - lz)
+    if (p.argmax) p.argmax[r] = t.i;
+    if (p.logp) {
+      const int y = p.tokens[r];
+      float xy = __builtin_nanf("");
+      if ((unsigned)y < (unsigned)p.V) {
+        if (p.bf16) {
+          const uint16_t h = *(const uint16_t*)(row + (int64_t)y * 2);
+          xy = __uint_as_float((uint32_t)h << 16);
+        } else {
+          xy = *(const float*)(row + (int64_t)y * 4);
+        }
+      }
+      p.logp[r] = xy - lz;
+    }
+  }
+}
+
+
+// ---------------------------------------------------------------------------------------
+// attention masses
+// ---------------------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+struct StatParams {
+  const __bf16* q;
+  const __bf16* kl;
+  const __bf16* kc;
+  const int32_t* seed_idx;
+  const int32_t* n_seed;
+  const float* lse;
+  const uint8_t* masked;
+  const uint8_t* drafted;
+  float* ws;  // [B, Hq, 2, Lr]: per head, d_in and d_out before the average over heads
+  float* d_in;
+  float* d_out;
+  int B, Hq, Hkv, L, d, max_seeds, group, r0, Lr, NB;
+  float scale;
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
+__device__ __forceinline__ f32x16 mfma16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+constexpr int kStatWaves = 8;
+
+template <int D>
+__global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const StatParams p) {
+  constexpr int KS = D / 16;
+  __shared__ uint32_t bits[COVER_MAX_L / 32];
+  __shared__ float sdin[kStatWaves][COVER_STATS_MAX_LR];  // per-wave d_in partials over its blocks
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hl = lane >> 5, l32 = lane & 31;
+  const int h = blockIdx.x % p.Hq, b = blockIdx.x / p.Hq;
+  const int g = h / p.group;
+  const int L = p.L;
+  // seed bitmap of this sequence; the d_in rows start at zero
+  const int nwords = (L + 31) >> 5;
+  for (int w = tid; w < nwords; w += 64 * kStatWaves) bits[w] = 0u;
+  for (int j = lane; j < p.Lr; j += 64) sdin[wave][j] = 0.0f;
+  __syncthreads();
+  int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
+  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+  for (int t = tid; t < ns; t += 64 * kStatWaves) {
+    const int j = p.seed_idx[(int64_t)b * p.max_seeds + t];
+    if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
+  }
+  __syncthreads();
+  auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
+
+  const __bf16* qbh = p.q + b * p.q_sb + h * p.q_sh;
+  const int64_t kvo = b * p.kv_sb + g * p.kv_sh;
+  const float* lrow = p.lse + ((int64_t)b * p.Hq + h) * L;
+  const float scale = p.scale;
+  // the K rows of key tile kt (this lane's row, d-chunks 2ks+hl; seeds from the cache)
+  auto load_k = [&](bf16x8* kf, int kt) {
+    const int kb = kt * 32;
+    const int kn = min(32, p.Lr - kb);
+    const int kj = p.r0 + kb + min(l32, kn - 1);
+    const __bf16* ksrc = (is_seed(kj) ? p.kc : p.kl) + kvo + (int64_t)kj * p.kv_sl;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = *(const bf16x8*)(ksrc + (2 * ks + hl) * 8);
+  };
+  for (int qb = wave; qb < p.NB; qb += kStatWaves) {
+    const int rb = qb * 32;                       // region offset of this query block
+    const int qn = min(32, p.Lr - rb);            // queries of the block inside the region
+    const int qi = p.r0 + rb + min(l32, qn - 1);  // this lane's query (clamped)
+    // Q operand: query qi, d-chunk 2ks+hl (also the A operand of S = Q K^T)
+    bf16x8 qf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qbh + (int64_t)qi * p.q_sl + (2 * ks + hl) * 8);
+    // live diagonal score of this lane's position, for seed rows
+    float s_live = 0.0f;
+    const bool own_seed = l32 < qn && is_seed(qi);
+    if (__builtin_amdgcn_ballot_w64(own_seed) != 0) {
+      const __bf16* kr = p.kl + kvo + (int64_t)qi * p.kv_sl;
+      float acc = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 kv = *(const bf16x8*)(kr + (2 * ks + hl) * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)qf[ks][e], (float)kv[e], acc);
+      }
+      s_live = acc + __shfl_xor(acc, 32);
+    }
+    // membership bits of the block's queries, and lse of the queries in S's registers
+    const uint64_t mq = __builtin_amdgcn_ballot_w64(l32 < qn && p.masked[(int64_t)b * p.Lr + rb + min(l32, qn - 1)] != 0) & 0xffffffffull;
+    const float lse_own = lrow[qi];
+    float lse_r[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) lse_r[r] = lrow[p.r0 + rb + min(8 * (r >> 2) + 4 * hl + (r & 3), qn - 1)];
+    float dout = 0.0f;  // this lane's query: sum over drafted keys (its 16 of each tile)
+    bf16x8 kf[KS], kn_f[KS];
+    load_k(kf, 0);
+    for (int kt = 0; kt < p.NB; ++kt) {
+      if (kt + 1 < p.NB) load_k(kn_f, kt + 1);  // the next tile's rows are requested first
+      const int kb = kt * 32;
+      const int kn = min(32, p.Lr - kb);
+      f32x16 st = {}, sq = {};  // S^T (lane = query, registers = keys), S (lane = key)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        st = mfma16(kf[ks], qf[ks], st);
+        sq = mfma16(qf[ks], kf[ks], sq);
+      }
+      const uint64_t dk = __builtin_amdgcn_ballot_w64(l32 < kn && p.drafted[(int64_t)b * p.Lr + kb + min(l32, kn - 1)] != 0) & 0xffffffffull;
+      const bool diag_tile = kt == qb;
+      float din = 0.0f;  // this lane's key: sum over masked queries (its 16 of the block)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 8 * (r >> 2) + 4 * hl + (r & 3);  // key (in st) / query (in sq) of register r
+        // seed rows see their own live key on the diagonal
+        float a = st[r], c = sq[r];
+        if (diag_tile && row == l32 && own_seed) { a = s_live; c = s_live; }
+        const float wt = __expf(a * scale - lse_own);
+        const float wq = __expf(c * scale - lse_r[r]);
+        dout += ((dk >> row) & 1) ? wt : 0.0f;
+        din += ((mq >> row) & 1) ? wq : 0.0f;
+      }
+      din += __shfl_xor(din, 32);
+      if (hl == 0 && l32 < kn) sdin[wave][kb + l32] += din;  // this wave's row only
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[ks] = kn_f[ks];
+    }
+    dout += __shfl_xor(dout, 32);
+    if (hl == 0 && l32 < qn) p.ws[(((int64_t)b * p.Hq + h) * 2 + 1) * p.Lr + rb + l32] = dout;
+  }
+  __syncthreads();
+  // d_in of this head: the waves' rows added in a fixed order
+  for (int j = tid; j < p.Lr; j += 64 * kStatWaves) {
+    float s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kStatWaves; ++w) s += sdin[w][j];
+    p.ws[(((int64_t)b * p.Hq + h) * 2 + 0) * p.Lr + j] = s;
+  }
+}
+
+// d_in(j) = (1/Hq) sum_h ws_in[h][j], d_out(j) = (1/Hq) sum_h ws_out[h][j], heads in order
+__global__ __launch_bounds__(256) void cover_attn_stats_reduce_kernel(const StatParams p) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= p.Lr) return;
+  const float* w = p.ws + (int64_t)b * p.Hq * 2 * p.Lr + j;
+  float din = 0.0f, dout = 0.0f;
+#pragma unroll 8
+  for (int h = 0; h < p.Hq; ++h) {
+    din += w[(int64_t)(2 * h) * p.Lr];
+    dout += w[(int64_t)(2 * h + 1) * p.Lr];
+  }
+  const float inv = 1.0f / (float)p.Hq;
+  p.d_in[(int64_t)b * p.Lr + j] = din * inv;
+  p.d_out[(int64_t)b * p.Lr + j] = dout * inv;
+}
+
+}  // namespace
+
+hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream) {
+  TokParams p;
+  p.logits = (const char*)a.logits;
+  p.tokens = a.tokens;
+  p.logp = a.logp;
+  p.conf = a.conf;
+  p.argmax = a.argmax;
+  p.row_stride_bytes = a.row_stride * (a.bf16 ? 2 : 4);
+  p.V = a.V;
+  p.bf16 = a.bf16;
+  hipLaunchKernelGGL(cover_token_stats_kernel, dim3((unsigned)a.R), dim3(kTokThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream) {
+  StatParams p;
+  p.q = (const __bf16*)a.q;
+  p.kl = (const __bf16*)a.k_live;
+  p.kc = (const __bf16*)a.k_cache;
+  p.seed_idx = a.seed_idx;
+  p.n_seed = a.n_seed;
+  p.lse = a.lse;
+  p.masked = a.masked;
+  p.drafted = a.drafted;
+  p.ws = a.workspace;
+  p.d_in = a.d_in;
+  p.d_out = a.d_out;
+  p.B = a.B; p.Hq = a.Hq; p.Hkv = a.Hkv; p.L = a.L; p.d = a.d; p.max_seeds = a.max_seeds;
+  p.group = a.Hq / a.Hkv;
+  p.r0 = a.r0; p.Lr = a.Lr;
+  p.NB = (a.Lr + 31) / 32;
+  p.scale = a.scale;
+  p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
+  p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
+  const int64_t nwg = (int64_t)a.B * a.Hq;
+  if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+  if (a.d == 128)
+    hipLaunchKernelGGL(cover_attn_stats_kernel<128>, dim3((unsigned)nwg), dim3(64 * kStatWaves), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cover_attn_stats_kernel<64>, dim3((unsigned)nwg), dim3(64 * kStatWaves), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(cover_attn_stats_reduce_kernel, dim3((unsigned)((a.Lr + 255) / 256), (unsigned)a.B),
+                     dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

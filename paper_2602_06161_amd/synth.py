@@ -166,3 +166,40 @@ def step_inputs(cfg: AttnConfig | str = "llada", seed: int = 0) -> dict:
     a["pos_offset"] = c.prompt
     a["Lr"] = Lr
     return a
+
+
+def token_inputs(R: int, V: int, seed: int = 0, dtype: str = "bf16", peak: float = 14.0) -> dict:
+    """Logits of R positions over a vocabulary of V (stand-in for the LM head's output on the
+    generated block): N(0, 2^2) with one token per row raised by U(0, peak), so the maximum
+    probability spans near-uniform to near-certain rows.  logits is a [R, V] view of
+    `buffer`, whose rows are padded to 16 bytes (move the buffer, then slice, to keep the
+    padded row stride on the device).  tokens: the raised token for even rows, a
+    uniformly random token for odd rows."""
+    rng = np.random.default_rng(seed + 104729)
+    x = rng.standard_normal(size=(R, V)).astype(np.float32) * 2.0
+    top = rng.integers(0, V, size=R)
+    x[np.arange(R), top] += rng.uniform(0.0, peak, size=R).astype(np.float32)
+    per = 8 if dtype == "bf16" else 4
+    stride = (V + per - 1) // per * per
+    buf = torch.zeros((R, stride), dtype=TORCH_DTYPE[dtype])
+    buf[:, :V] = torch.from_numpy(x).to(TORCH_DTYPE[dtype])
+    tokens = np.where(np.arange(R) % 2 == 0, top, rng.integers(0, V, size=R)).astype(np.int32)
+    return dict(logits=buf[:, :V], buffer=buf, tokens=torch.from_numpy(tokens))
+
+
+def stats_inputs(cfg: AttnConfig | str = "llada", seed: int = 0, n_draft: int = 15) -> dict:
+    """Attention inputs plus the masks of the generated region [prompt, L): masked = the
+    positions still masked, drafted = up to n_draft of them chosen uniformly."""
+    a = attn_inputs(cfg, seed)
+    c = a["cfg"]
+    rng = np.random.default_rng(seed + 15485863)
+    Lr = c.L - c.prompt
+    masked = (~a["unmasked"].numpy()[:, c.prompt:]).astype(np.uint8)
+    drafted = np.zeros_like(masked)
+    for b in range(c.B):
+        mpos = np.nonzero(masked[b])[0]
+        if mpos.size:
+            drafted[b, rng.choice(mpos, size=min(n_draft, mpos.size), replace=False)] = 1
+    a.update(masked=torch.from_numpy(masked), drafted=torch.from_numpy(drafted), r0=c.prompt,
+             Lr=Lr)
+    return a

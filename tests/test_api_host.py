@@ -113,3 +113,60 @@ def test_select_errors():
     assert _sel(cover.SelectDesc(**good), sc=FAKE + 4) == cover.COVER_ERR_INVALID
     assert _sel(cover.SelectDesc(**{**good, "pos_offset": 0x7fffff00})) == cover.COVER_ERR_INVALID
     assert _sel(cover.SelectDesc(**{**good, "B": 0}), lp=None, fl=None, si=None, ns=None) == cover.COVER_OK
+
+
+def _tok(desc, logits=FAKE, tokens=FAKE, logp=FAKE):
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return cover.lib().cover_token_stats(p(logits), p(tokens), p(logp), None, None,
+                                         None if desc is None else ctypes.byref(desc), None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(R=-1), cover.COVER_ERR_INVALID),
+    (dict(V=0), cover.COVER_ERR_INVALID),
+    (dict(row_stride=100), cover.COVER_ERR_INVALID),       # < V
+    (dict(row_stride=1004), cover.COVER_ERR_INVALID),      # 2008 bytes: not a multiple of 16
+    (dict(dtype=7), cover.COVER_ERR_INVALID),
+])
+def test_token_stats_rejects_bad_descriptors(kw, expect):
+    d = dict(R=4, V=1000, dtype=cover.COVER_BF16, row_stride=1008)
+    d.update(kw)
+    assert _tok(cover.TokenDesc(**d)) == expect
+
+
+def test_token_stats_rejects_bad_pointers():
+    good = cover.TokenDesc(4, 1000, cover.COVER_BF16, 1008)
+    assert _tok(None) == cover.COVER_ERR_INVALID
+    assert _tok(good, logits=None) == cover.COVER_ERR_INVALID
+    assert _tok(good, logits=FAKE + 8) == cover.COVER_ERR_INVALID   # not 16-byte aligned
+    assert _tok(good, tokens=None) == cover.COVER_ERR_INVALID       # logp wanted, no tokens
+    assert _tok(cover.TokenDesc(0, 1000, cover.COVER_BF16, 1008), logits=None) == cover.COVER_OK
+
+
+def _stats(desc, ws=FAKE, lse=FAKE):
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return cover.lib().cover_attn_stats(p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(lse),
+                                        p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(ws),
+                                        None if desc is None else ctypes.byref(desc), None)
+
+
+@pytest.mark.parametrize("kw,r0,Lr,expect", [
+    (dict(), -1, 8, cover.COVER_ERR_INVALID),
+    (dict(), 60, 8, cover.COVER_ERR_INVALID),               # r0 + Lr > L
+    (dict(), 0, -1, cover.COVER_ERR_INVALID),
+    (dict(dtype=cover.COVER_F32), 0, 8, cover.COVER_ERR_UNSUPPORTED),
+    (dict(d=96), 0, 8, cover.COVER_ERR_UNSUPPORTED),
+    (dict(Hkv=3), 0, 8, cover.COVER_ERR_INVALID),
+    (dict(), 0, 0, cover.COVER_OK),                         # empty region: no-op
+    (dict(L=4096), 0, 2049, cover.COVER_ERR_UNSUPPORTED),   # region longer than the LDS rows
+])
+def test_attn_stats_rejects_bad_descriptors(kw, r0, Lr, expect):
+    assert _stats(cover.StatsDesc(_good(**kw), r0, Lr)) == expect
+
+
+def test_attn_stats_rejects_missing_buffers():
+    good = cover.StatsDesc(_good(), 0, 8)
+    assert _stats(None) == cover.COVER_ERR_INVALID
+    assert _stats(good, ws=None) == cover.COVER_ERR_INVALID
+    assert _stats(good, lse=None) == cover.COVER_ERR_INVALID
+    assert cover.attn_stats_workspace(1, 32, 256) == 32 * 2 * 256
