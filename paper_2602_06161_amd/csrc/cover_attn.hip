@@ -572,6 +572,10 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
   sML[(wave * 2 + 0) * 64 + lane] = m;
   sML[(wave * 2 + 1) * 64 + lane] = lsum;
   __syncthreads();
+  // The finished d-half of the wave's 32 rows (bf16), in O^T order: entry dbh*4+g4 holds
+  // columns dbh*32 + g4*8 + hl*4 .. +3 of the half for row l32.
+  bf16x4 outv[DBH * 4];
+  float mm_out = 0.0f, ltot_out = 1.0f;
   auto finish = [&](auto half) {
     constexpr int HF = decltype(half)::value;  // d-half finalised here
     // seed rows: the live diagonal term, one more element of the row's softmax
@@ -582,38 +586,57 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_bf16_kernel(const Para
     const float fd = __builtin_amdgcn_exp2f(td - mm);
     const float ltot = lsum * fa + lb * fb + fd;
     const float inv = 1.0f / ltot;
-    const int qf = qw + l32;
-    if (qf < L) {
-      __bf16* orow = p.out + b * p.q_sb + h * p.q_sh + (int64_t)qf * p.q_sl;
+    mm_out = mm;
+    ltot_out = ltot;
 #pragma unroll
-      for (int dbh = 0; dbh < DBH; ++dbh) {
-        const int db = HF * DBH + dbh;
+    for (int dbh = 0; dbh < DBH; ++dbh) {
+      const int db = HF * DBH + dbh;
 #pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int d0 = db * 32 + g4 * 8 + hl * 4;
-          const f32x4 tv = *(const f32x4*)(theirs + (dbh * 4 + g4) * 256 + lane * 4);
-          f32x4 v;
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = db * 32 + g4 * 8 + hl * 4;
+        const f32x4 tv = *(const f32x4*)(theirs + (dbh * 4 + g4) * 256 + lane * 4);
+        f32x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = o[db][g4 * 4 + e] * fa + tv[e] * fb;
-          if (block_seeded) {
-            typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-            const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
-                dg + l32 * T::ROW + ((((d0 >> 3) ^ k_swz<T::ROW>(l32))) << 4) + (d0 & 7) * 2);
-            v[0] += fd * bf16_lo(raw[0]);
-            v[1] += fd * bf16_hi(raw[0]);
-            v[2] += fd * bf16_lo(raw[1]);
-            v[3] += fd * bf16_hi(raw[1]);
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] *= inv;
-          *(bf16x4*)(orow + d0) = __builtin_convertvector(v, bf16x4);
+        for (int e = 0; e < 4; ++e) v[e] = o[db][g4 * 4 + e] * fa + tv[e] * fb;
+        if (block_seeded) {
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
+              dg + l32 * T::ROW + ((((d0 >> 3) ^ k_swz<T::ROW>(l32))) << 4) + (d0 & 7) * 2);
+          v[0] += fd * bf16_lo(raw[0]);
+          v[1] += fd * bf16_hi(raw[0]);
+          v[2] += fd * bf16_lo(raw[1]);
+          v[3] += fd * bf16_hi(raw[1]);
         }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] *= inv;
+        outv[dbh * 4 + g4] = __builtin_convertvector(v, bf16x4);
       }
-      if (p.lse && hl == 0 && kp == 0)
-        p.lse[((int64_t)b * p.Hq + h) * L + qf] = (mm + __builtin_amdgcn_logf(ltot)) * kLn2;
     }
   };
   if (kp) finish(IC<1>{}); else finish(IC<0>{});
+  if (p.lse && hl == 0 && kp == 0 && qw + l32 < L)
+    p.lse[((int64_t)b * p.Hq + h) * L + qw + l32] = (mm_out + __builtin_amdgcn_logf(ltot_out)) * kLn2;
+  // Stores: the half-rows go through an LDS tile (rows padded to keep 16-byte alignment and
+  // spread banks) so that each global store writes whole 128-byte lines of consecutive
+  // columns instead of 8-byte pieces of 32 rows.
+  __syncthreads();  // every wave has read its partner's merge slot
+  constexpr int TROW = D + 16;                     // bytes per tile row: D/2 columns + pad
+  static_assert(32 * TROW <= NJH * 64 * 4, "the output tile must fit a merge slot");
+  lds_t* const tile = (lds_t*)slot(wave);          // this wave's slot, now free
+#pragma unroll
+  for (int dbh = 0; dbh < DBH; ++dbh)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      *(__attribute__((address_space(3))) bf16x4*)(tile + l32 * TROW + (dbh * 32 + g4 * 8 + hl * 4) * 2) = outv[dbh * 4 + g4];
+  constexpr int CPR = D / 16;          // 16-byte chunks per half-row
+  constexpr int NRD = 32 * CPR / 64;   // reads (and stores) per lane
+  __bf16* const obase = p.out + b * p.q_sb + h * p.q_sh + kp * (D / 2);
+#pragma unroll
+  for (int it = 0; it < NRD; ++it) {
+    const int idx = it * 64 + lane, row = idx / CPR, ch = idx % CPR;
+    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(tile + row * TROW + ch * 16);
+    if (qw + row < L) *(u32x4*)(obase + (int64_t)(qw + row) * p.q_sl + ch * 8) = v;
+  }
 }
 
 // ----------------------------------------------------------------------------------------
