@@ -32,6 +32,7 @@ COMMON = [
 SOURCES = {
     "api.cpp": ["-x", "hip"],
     "cover_attn.hip": [],
+    "cover_attn_w4.hip": [],
     "cover_select.hip": ["-ffp-contract=off"],  # the selection is bit-exact fp64
     "cover_stats.hip": [],
 }

@@ -1,0 +1,836 @@
+// COVER attention on gfx950, head dimension 128, bf16: four waves per workgroup, one per SIMD.
+//
+// Same operation as the eight-wave kernel (arXiv 2602.06161, Sec. 5.1 "KV cache override" and
+// "Diagonal correction"; App. B): for query row i of batch row b with seed set S_b,
+//   K'_j = k_cache_j if j in S_b else k_live_j (V' likewise); row i attends to K' except that a
+//   seed row sees its own live key/value on the diagonal; out_i = softmax(scale q_i K^(i)) V^(i).
+// The diagonal is handled as in the eight-wave kernel: the cached diagonal score of a seed row
+// gets no weight in the main loop, and the live diagonal term exp(scale q_i.k_live_i) v_live_i
+// joins the row's softmax in the epilogue (exactly the leave-one-out row of App. B.1, with no
+// division by the closed form's r_i).
+//
+// Layout (one workgroup = 128 queries of one (b, h); wave w: query block qb = w & 1 of 64
+// queries, key half kh = w >> 1 of every 64-key stage):
+//   * S^T = K Q^T per 32-query tile (v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q from
+//     registers) and O^T += V^T P^T (A = V^T by ds_read_b64_tr_b16, B = P from the S^T
+//     registers).  A wave owns two 32-query tiles, so every K or V^T operand read from LDS
+//     feeds two MFMAs: a stage costs the workgroup 64 KiB of LDS reads (the transposing V read
+//     delivers about a third of the bandwidth of a plain 16-byte read), not 128 KiB.
+//   * The 128 O^T accumulators per lane live in AGPRs (one wave per SIMD has 512 registers);
+//     S, P and Q stay in VGPRs.
+//   * K/V stages go global -> LDS directly (global_load_lds_dwordx4, no VGPR staging), three
+//     buffers each, issued two stages ahead of their use; each row's source (live or cache)
+//     comes from the seed bitmap, clean stages use one uniform base.
+//   * Softmax without a running max: every row keeps the reference max of its first stage.
+//     A lane's per-stage probability sum above 2^24 (or not finite) flags the workgroup, which
+//     then recomputes its tile with an exact per-stage rescaling pass.  The flag never fires
+//     unless a later score exceeds the first stage's maximum by more than 24 in log2 units.
+//   * Waves w and w ^ 2 hold the same queries over the two key halves; they exchange one
+//     32-query tile each through LDS at the end, so each wave finishes 32 complete rows.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace cover {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+typedef __attribute__((address_space(3))) char lds_t;
+typedef __attribute__((address_space(1))) const char gmem_t;
+
+constexpr int kD = 128;
+constexpr int kRow = 2 * kD;                 // bytes per K/V row
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBM = 128;                     // queries per workgroup
+constexpr int kStage = 64;                   // keys per stage
+constexpr int kSBytes = kStage * kRow;       // one K or V stage buffer (16 KiB)
+constexpr int kLoads = kSBytes / 1024 / kWaves;  // 1-KiB loads per wave per stage buffer
+constexpr int kKS = kD / 16;                 // k-steps of S^T = K Q^T
+constexpr int kDB = kD / 32;                 // 32-row blocks of O^T
+constexpr float kInitMax = -1.0e30f;         // finite "no key seen yet" reference max
+constexpr float kBig = 16777216.0f;          // 2^24
+constexpr float kLn2 = 0.693147180559945309f;
+static_assert(kLoads == 4, "a stage gives every wave four 1-KiB loads");
+
+// s_waitcnt immediates that wait for vmcnt <= n only (lgkmcnt and expcnt untouched)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xf00; }
+// at the top of a step the eight loads of the previous step may stay in flight
+constexpr int kWaitStep = vmcnt_imm(2 * kLoads);
+
+struct Params4 {
+  const __bf16* q;
+  const __bf16* kl;
+  const __bf16* vl;
+  const __bf16* kc;
+  const __bf16* vc;
+  const int32_t* seed_idx;
+  const int32_t* n_seed;
+  __bf16* out;
+  float* lse;
+  int B, Hq, Hkv, L, max_seeds, group, n_qt, xcd_slots;
+  float c2;  // scale * log2(e)
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
+// LDS swizzles (64 banks of 4 bytes).  K rows: the 16-byte chunk index is XOR-ed with row % 16,
+// so the 32 rows of one b128 operand read spread over all banks.  V rows: the chunk index is
+// XOR-ed with 4 * (row % 4), so one transposing read (8 rows x 64 bytes) covers every bank
+// exactly twice.
+__device__ __forceinline__ int k_swz(int row) { return row & 15; }
+__device__ __forceinline__ int v_swz(int row) { return (row & 3) << 2; }
+__device__ __forceinline__ uint32_t k_off(int row, int c) { return row * kRow + ((c ^ k_swz(row)) << 4); }
+__device__ __forceinline__ uint32_t v_elem(int row, int col) {
+  return row * kRow + (((col >> 3) ^ v_swz(row)) << 4) + ((col & 7) << 1);
+}
+
+// The MFMAs are written as inline assembly so that the register class of each accumulator is
+// fixed: S in VGPRs (read by the softmax), O in AGPRs (touched by VALU code only at the end).
+// The compiler does not see these as MFMAs, so the few places where VALU code reads an MFMA
+// result soon after it was written wait explicitly (mfma_drain).
+__device__ __forceinline__ void mfma_first(f32x16& d, bf16x8 a, bf16x8 qb) {  // d = a q
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(qb));
+}
+__device__ __forceinline__ void mfma_v(f32x16& d, bf16x8 a, bf16x8 qb) {  // d += a q (VGPR)
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(qb));
+}
+__device__ __forceinline__ void mfma_a(f32x16& d, bf16x8 a, bf16x8 b) {  // d += a b (AGPR)
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(d) : "v"(a), "v"(b));
+}
+// wait until every issued MFMA has written its result (the 8-pass 32x32x16 MFMA needs at
+// most 18 wait states before a dependent VALU read; 3 x 8 are given)
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
+// VALU-written operands need 2 wait states before an MFMA reads them; tying the nop to the
+// operand orders it after the write and before the read
+__device__ __forceinline__ void valu_to_mfma(bf16x8& x) { asm("s_nop 1" : "+v"(x)); }
+__device__ __forceinline__ u32x4 lds_read16(const lds_t* p) {
+  return *(const __attribute__((address_space(3))) u32x4*)p;
+}
+__device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+}
+// global -> LDS, 16 bytes per lane: lane l's bytes land at LDS byte lds + 16 l (lds uniform).
+// Inline assembly, so the compiler does not track these loads: every read of their data is
+// preceded by an explicit vmcnt wait of the issuing wave and a barrier.
+__device__ __forceinline__ uint32_t lds_u32(const lds_t* ptr) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ptr);
+}
+__device__ __forceinline__ void dma_s(uint32_t lds, gmem_t* sbase, uint32_t voff) {  // uniform base
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds), "v"(voff), "s"(sbase) : "memory", "m0");
+}
+__device__ __forceinline__ void dma_v(uint32_t lds, gmem_t* addr) {  // per-lane address
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(lds), "v"((uint64_t)addr) : "memory", "m0");
+}
+__device__ __forceinline__ float swap_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float swap_add(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float fmax3(float a, float b, float c) { return __builtin_fmaxf(__builtin_fmaxf(a, b), c); }
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float lane_max(const f32x16& s) {
+  const float a = fmax3(s[0], s[1], s[2]), b = fmax3(s[3], s[4], s[5]);
+  const float c = fmax3(s[6], s[7], s[8]), d = fmax3(s[9], s[10], s[11]);
+  const float e = fmax3(s[12], s[13], s[14]);
+  return fmax3(fmax3(a, b, c), __builtin_fmaxf(d, e), s[15]);
+}
+__device__ __forceinline__ gmem_t* uniform_ptr(const void* ptr) {
+  const uint64_t v = (uint64_t)ptr;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (gmem_t*)(((uint64_t)hi << 32) | lo);
+}
+
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
+
+__global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params4 p) {
+  // three K and three V stage buffers; the live value rows of the seed rows' diagonals; the
+  // seed bitmap of the sequence and its per-stage summary; merge scalars; the recompute flag
+  __shared__ __attribute__((aligned(1024))) char sK0[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sK1[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sK2[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sV0[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sV1[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sV2[kSBytes];
+  __shared__ __attribute__((aligned(1024))) char sDiag[kWaves * 32 * kRow];
+  __shared__ uint32_t bits[COVER_MAX_L / 32];
+  __shared__ uint32_t sdirty[COVER_MAX_L / kStage / 32];
+  __shared__ __attribute__((aligned(16))) float sML[kWaves * 2 * 64];
+  __shared__ uint32_t sbad;
+  auto kbuf = [&](int n) __attribute__((always_inline)) -> lds_t* { return (lds_t*)(n == 0 ? sK0 : (n == 1 ? sK1 : sK2)); };
+  auto vbuf = [&](int n) __attribute__((always_inline)) -> lds_t* { return (lds_t*)(n == 0 ? sV0 : (n == 1 ? sV1 : sV2)); };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qb = wave & 1;   // 64-query block
+  const int kh = wave >> 1;  // key half of every stage; also the query tile this wave finishes
+  const int hl = lane >> 5, l32 = lane & 31;
+
+  // ---- workgroup -> (b, h, query tile); consecutive logical tiles share an XCD ------------
+  int li = blockIdx.x;
+  if (p.xcd_slots > 0) li = (li & 7) * p.xcd_slots + (li >> 3);
+  const int qt = li % p.n_qt;
+  const int bh = li / p.n_qt;
+  const int h = bh % p.Hq, b = bh / p.Hq;
+  const int g = h / p.group;
+  const int L = p.L;
+  const int q0 = qt * kBM;
+  const int qw = q0 + qb * 64;  // first query of this wave's block
+  const __bf16* qbase = p.q + b * p.q_sb + h * p.q_sh;
+  const int64_t kvoff = b * p.kv_sb + g * p.kv_sh;
+  const int n_it = (L + kStage - 1) / kStage;
+  const int64_t sbase = (int64_t)b * p.max_seeds;
+
+  // ---- seed list first: the loads below complete in order, so its wait is short ----------
+  int ns = 0;
+  if (p.max_seeds > 0) ns = p.n_seed[b];
+  const int sj0 = tid < p.max_seeds ? p.seed_idx[sbase + tid] : -1;
+
+  // ---- stage loads ---------------------------------------------------------------------
+  // Load j of this wave covers stage rows (wave * 4 + j) * 4 + lane / 16, physical chunk
+  // lane % 16 (logical chunk = physical ^ swizzle), landing at byte (wave * 4 + j) * 1024 +
+  // 16 lane of the stage buffer, which is where the swizzled layout wants it.
+  auto ld_row = [&](int j) __attribute__((always_inline)) { return (wave * kLoads + j) * 4 + (lane >> 4); };
+  auto ld_chunk = [&](int j, bool is_v) __attribute__((always_inline)) -> uint32_t {
+    const int row = ld_row(j), pc = lane & 15;
+    return (uint32_t)((pc ^ (is_v ? v_swz(row) : k_swz(row))) << 4);
+  };
+  const int64_t row_bytes = p.kv_sl * 2;
+  const int64_t stage_bytes = kStage * row_bytes;
+  uint32_t offK[kLoads], offV[kLoads];
+#pragma unroll
+  for (int j = 0; j < kLoads; ++j) {
+    offK[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, false);
+    offV[j] = (uint32_t)(ld_row(j) * row_bytes) + ld_chunk(j, true);
+  }
+  gmem_t* const klb = uniform_ptr(p.kl + kvoff);
+  gmem_t* const kcb = uniform_ptr(p.kc + kvoff);
+  gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
+  gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
+  auto clamp_stage = [=](int i) __attribute__((always_inline)) -> int { return i < n_it ? i : n_it - 1; };
+  auto wdst = [&](lds_t* buf, int j) __attribute__((always_inline)) -> lds_t* { return buf + (wave * kLoads + j) * 1024; };
+  // speculative loads from the live tensors, rows past L clamped
+  auto ld_live = [&](lds_t* buf, gmem_t* live, bool is_v, int stage) __attribute__((always_inline)) {
+    const int kb = stage * kStage;
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int key = min(kb + ld_row(j), L - 1);
+      dma_v(lds_u32(wdst(buf, j)), live + key * row_bytes + ld_chunk(j, is_v));
+    }
+  };
+  // K(0); Q; V(0), K(1); V(1), K(2)
+  ld_live(kbuf(0), klb, false, 0);
+
+  // ---- Q fragments: tile t, query qw + 32 t + l32, d-chunk 2 ks + hl --------------------
+  bf16x8 qreg[2][kKS];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int qi = min(qw + 32 * t + l32, L - 1);
+    const __bf16* qrow = qbase + (int64_t)qi * p.q_sl + hl * 8;
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) qreg[t][ks] = *(const bf16x8*)(qrow + ks * 16);
+  }
+  // The live key rows of this wave's diagonal tile, loaded for every tile before the seeds
+  // are known (they are L2-resident: the same rows are K rows of this head): a seed row needs
+  // its raw live diagonal score q_i . k_live_i (lane pair halves of d, summed by a swap).
+  u32x4 klive[kKS];
+  {
+    const int qr = min(qw + 32 * kh + l32, L - 1);
+    const uint32_t* krow = (const uint32_t*)(p.kl + kvoff + (int64_t)qr * p.kv_sl + hl * 8);
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) klive[ks] = *(const u32x4*)(krow + ks * 8);
+  }
+  ld_live(vbuf(0), vlb, true, 0);
+  ld_live(kbuf(1), klb, false, clamp_stage(1));
+  ld_live(vbuf(1), vlb, true, clamp_stage(1));
+  ld_live(kbuf(2), klb, false, clamp_stage(2));
+  // the seed list, K(0), Q and the live diagonal rows have landed once no more than the
+  // sixteen stage loads issued after them are outstanding
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * kLoads));
+
+
+  // ---- seed bitmap of this sequence -----------------------------------------------------
+  const int nwords = (L + 31) >> 5;
+  // words past the sequence are cleared too: per-stage lookups read two words per stage
+  for (int w = tid; w < 2 * n_it; w += kThreads) bits[w] = 0u;
+  if (tid < COVER_MAX_L / kStage / 32) sdirty[tid] = 0u;
+  if (tid == 0) sbad = 0u;
+  __syncthreads();
+  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+  auto mark = [&](int j) __attribute__((always_inline)) {
+    atomicOr(&bits[j >> 5], 1u << (j & 31));
+    atomicOr(&sdirty[j >> 11], 1u << ((j >> 6) & 31));
+  };
+  if (tid < ns && (unsigned)sj0 < (unsigned)L) mark(sj0);
+  for (int t = tid + kThreads; t < ns; t += kThreads) {
+    const int j = p.seed_idx[sbase + t];
+    if ((unsigned)j < (unsigned)L) mark(j);
+  }
+  __syncthreads();
+  auto is_seed = [&](int j) __attribute__((always_inline)) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
+
+  // Lane l holds the seed flags of stages 64 l .. 64 l + 63 (two words); a stage's flag is
+  // read back with a lane read.
+  const uint32_t dirty_lo = sdirty[(2 * lane) & (COVER_MAX_L / kStage / 32 - 1)];
+  const uint32_t dirty_hi = sdirty[(2 * lane + 1) & (COVER_MAX_L / kStage / 32 - 1)];
+  auto dirty = [&](int stage) __attribute__((always_inline)) -> bool {
+    const uint32_t w = ((stage >> 5) & 1) ? __builtin_amdgcn_readlane(dirty_hi, stage >> 6)
+                                          : __builtin_amdgcn_readlane(dirty_lo, stage >> 6);
+    return (w >> (stage & 31)) & 1u;
+  };
+  const int spC = L % kStage != 0 ? n_it - 1 : -1;  // ragged last stage
+
+  // Issue the loads of one stage of K or V.  Stages without seeds and within L use a uniform
+  // base and per-lane 32-bit offsets; the others choose each row's source and clamp rows past L.
+  auto ld = [&](lds_t* buf, gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v,
+                int stage_in) __attribute__((always_inline)) {
+    const int stage = __builtin_amdgcn_readfirstlane(stage_in);
+    if (stage != spC && !dirty(stage)) {
+      gmem_t* lb = uniform_ptr((const void*)(live + stage * stage_bytes));
+#pragma unroll
+      for (int j = 0; j < kLoads; ++j) dma_s(lds_u32(wdst(buf, j)), lb, off[j]);
+    } else {
+      const int kb = stage * kStage;
+#pragma unroll
+      for (int j = 0; j < kLoads; ++j) {
+        const int key = min(kb + ld_row(j), L - 1);
+        gmem_t* src = is_seed(key) ? cache : live;
+        dma_v(lds_u32(wdst(buf, j)), src + key * row_bytes + ld_chunk(j, is_v));
+      }
+    }
+  };
+
+  // After the uniform loads of a stage (issued earlier by the same wave, so they land first),
+  // reload the rows that need another source: seed rows from the cache, and in the ragged
+  // last stage the rows below L (the uniform loads read the last 64 rows there).  Only the
+  // lanes of such rows take part.
+  auto patch = [&](lds_t* buf, gmem_t* live, gmem_t* cache, const uint32_t* off, int stage_in)
+                   __attribute__((always_inline)) {
+    const int st = __builtin_amdgcn_readfirstlane(stage_in);
+    gmem_t* lb = uniform_ptr((const void*)(live + st * stage_bytes));
+    gmem_t* cb = uniform_ptr((const void*)(cache + st * stage_bytes));
+    const bool ragged = st == spC;
+    const uint64_t sm = ((uint64_t)bits[2 * st + 1] << 32) | bits[2 * st];  // the stage's seeds
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int r = ld_row(j);
+      const bool in = st * kStage + r < L;
+      if (ragged && in) dma_s(lds_u32(wdst(buf, j)), lb, off[j]);
+      if (in && ((sm >> r) & 1u)) dma_s(lds_u32(wdst(buf, j)), cb, off[j]);
+    }
+  };
+
+  // ---- diagonal set-up --------------------------------------------------------------------
+  // Query tile kh of this wave (queries qd0 + c) has its diagonal keys in stage sd, key half
+  // kh, tile row c: lane half (c / 4) % 2, register (c / 8) * 4 + c % 4.
+  const int qd0 = qw + 32 * kh;
+  const int sd = qw / kStage;
+  const bool holds_diag = hl == ((l32 >> 2) & 1);
+  const int rd = ((l32 >> 3) << 2) | (l32 & 3);
+  const bool qd_seed = (qd0 + l32) < L && is_seed(qd0 + l32);
+  const bool diag_seed = holds_diag && qd_seed;
+  const bool block_seeded = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
+  const int spA = block_seeded ? sd : -1;
+  auto is_special = [=](int i) __attribute__((always_inline)) -> bool { return (i == spA) | (i == spC); };
+  // uniform base of a stage's rows for the in-loop loads: the ragged last stage reads the
+  // last 64 rows instead (in bounds; it is then reloaded row by row)
+  auto clean_base = [&](gmem_t* live, int stage) __attribute__((always_inline)) -> gmem_t* {
+    const int64_t off = stage == spC ? (int64_t)(L - kStage) * row_bytes : stage * stage_bytes;
+    return uniform_ptr((const void*)(live + off));
+  };
+
+  // Stages 0..2 were loaded from the live tensors before the seeds were known; reload the
+  // ones that hold seeds (after every wave's speculative loads have landed).
+  {
+    const bool redo = dirty(0) || dirty(clamp_stage(1)) || dirty(clamp_stage(2));
+    if (redo) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      ld(kbuf(0), klb, kcb, offK, false, 0);
+      ld(vbuf(0), vlb, vcb, offV, true, 0);
+      ld(kbuf(1), klb, kcb, offK, false, clamp_stage(1));
+      ld(vbuf(1), vlb, vcb, offV, true, clamp_stage(1));
+      ld(kbuf(2), klb, kcb, offK, false, clamp_stage(2));
+    }
+  }
+  // Seed rows of the diagonal tile: their live value rows (K swizzle) and the raw live
+  // diagonal score q_i . k_live_i (lane pair halves of d, summed by a swap).
+  lds_t* const dg = (lds_t*)sDiag + wave * (32 * kRow);
+  if (block_seeded) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = j * 4 + (lane >> 4), pc = lane & 15;
+      const int vr = min(qd0 + row, L - 1);
+      dma_v(lds_u32(dg + j * 1024), vlb + vr * row_bytes + ((pc ^ k_swz(row)) << 4));
+    }
+  }
+  // (computed on every path: a load left unconsumed on one path would make the compiler wait
+  // for all memory operations at the next write of its registers, inside the main loop)
+  float s_live;
+  {
+    float acc = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const u32x4 kv = klive[ks];
+      const bf16x8 q0v = qreg[0][ks], q1v = qreg[1][ks];
+      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
+        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
+      }
+    }
+    s_live = swap_add(acc);
+  }
+
+  // Q moves to AGPRs for good (the B operand of S^T = K Q^T may come from either file; the
+  // VGPRs are needed for S, P and the operands read from LDS)
+  bf16x8 qa[2][kKS];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) asm volatile("; Q to AGPR" : "=a"(qa[t][ks]) : "0"(qreg[t][ks]));
+
+  // ---- per-lane LDS read addresses (relative to a stage buffer) ---------------------------
+  uint32_t kaddr[kKS];
+#pragma unroll
+  for (int ks = 0; ks < kKS; ++ks) kaddr[ks] = k_off(kh * 32 + l32, 2 * ks + hl);
+  // A operand of O^T += V^T P^T for keys kh*32 + 16 kk + {0..3, 8..11} + 4 (G / 2), d-block
+  // db: lane (G = lane / 16, i = lane % 16) reads V[row][db*32 + 16 (G % 2) + 4 (i % 4) .. +3]
+  // with row = kh*32 + 16 kk + 4 (G / 2) + i / 4 (+8 for the upper half); the same key order
+  // the S^T registers give the P^T operand.  kk and the +8 move the row by multiples of 4,
+  // which leave the swizzle unchanged: constant offsets.
+  uint32_t vaddr[kDB];
+  {
+    const int G = lane >> 4, ii = lane & 15;
+    const int row = kh * 32 + 4 * (G >> 1) + (ii >> 2);
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) vaddr[db] = v_elem(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
+  }
+
+  // ---- the three compute pieces ------------------------------------------------------------
+  auto qk = [&](const lds_t* kb, f32x16* s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
+      if (ks == 0) {
+        mfma_first(s[0], a, qa[0][ks]);
+        mfma_first(s[1], a, qa[1][ks]);
+      } else {
+        mfma_v(s[0], a, qa[0][ks]);
+        mfma_v(s[1], a, qa[1][ks]);
+      }
+    }
+  };
+  // keys of this wave's half of `stage` past L, and the seed rows' own (cached) column, get no
+  // weight; the live diagonal term joins in the epilogue
+  auto special_fix = [&](int stage, f32x16* s) __attribute__((always_inline)) {
+    if (stage * kStage + kStage > L) {
+      const int kbase = stage * kStage + kh * 32;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool ok = kbase + ((r >> 2) << 3) + hl * 4 + (r & 3) < L;
+          s[t][r] = ok ? s[t][r] : -INFINITY;
+        }
+    }
+    if (block_seeded && stage == sd) {
+      // tile kh holds the diagonal; both tiles are written with value selects only (a
+      // branch per tile would make the compiler address the tiles through memory)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[t][r] = (kh == t && diag_seed && r == rd) ? -INFINITY : s[t][r];
+    }
+  };
+
+  float m[2], lsum[2] = {0.0f, 0.0f};
+  f32x16 o[2][kDB];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) o[t][db] = (f32x16){};
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // exp2(c2 s - m) -> bf16 P (both tiles), row sums of the bf16 weights as the MFMA sees them;
+  // returns the lanes whose per-stage sum left the safe range
+  auto softmax = [&](const f32x16* s, bf16x8 (*pk)[2], float* mref) __attribute__((always_inline)) -> uint64_t {
+    uint64_t bad = 0;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const float nm = -mref[t];
+      f32x16 pr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], p.c2, nm));
+      pk[t][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
+      pk[t][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+      float ls[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8 w = pk[t][kk];
+        float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, 0.0f, false);
+        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, a, false);
+        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, a, false);
+        ls[kk] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, a, false);
+      }
+      const float st = ls[0] + ls[1];
+      lsum[t] += st;
+      bad |= __builtin_amdgcn_ballot_w64(!(st <= kBig));
+    }
+    return bad;
+  };
+  auto pv = [&](const lds_t* vb, bf16x8 (*pk)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) valu_to_mfma(pk[t][kk]);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int db = 0; db < kDB; ++db) {
+        const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
+        const i16x8 v = __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, v);
+        mfma_a(o[0][db], a, pk[0][kk]);
+        mfma_a(o[1][db], a, pk[1][kk]);
+      }
+    }
+  };
+
+  // The main block of a step: S(i+1) = K(i+1) Q^T, softmax of S(i), O += P(i) V(i), written
+  // in issue order (the MFMAs keep their order; LDS reads stay where they are written, ahead
+  // of their use): K operands four k-steps ahead, V operands one d-block ahead; the softmax
+  // elements of the first key half of both tiles go between the S MFMAs, so that the P of
+  // the first PV half is ready when the S MFMAs end.
+  // The main block of a step: S(i+1) = K(i+1) Q^T - m, softmax of S(i), O += P(i) V(i), and
+  // the loads of K(i+3) and V(i+2), written in issue order (the MFMAs keep their order; LDS
+  // reads and global loads stay where they are written): K operands four k-steps ahead, V
+  // operands one d-block ahead, one global load between MFMA pairs (a burst of eight stalls
+  // the issuing wave on the vector-memory queue); the exponentials of the first key half of
+  // both tiles go between the S MFMAs, so that the P of the first PV half is ready when they
+  // end.
+  auto fused = [&](const lds_t* kb, f32x16* sn, const f32x16* sc, const lds_t* vb, lds_t* kdst,
+                   gmem_t* kg, lds_t* vdst, gmem_t* vg) __attribute__((always_inline)) -> uint64_t {
+    bf16x8 ka[kKS];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) ka[ks] = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
+    const float nm[2] = {-m[0], -m[1]};
+    f32x16 pr[2];
+    auto expo = [&](int e) __attribute__((always_inline)) {  // element e of the order below
+      const int t = (e >> 3) & 1, r = (e & 7) + ((e >> 4) << 3);
+      pr[t][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][r], p.c2, nm[t]));
+    };
+    bf16x8 va[2][kDB];
+    auto vread = [&](int kk, int db) __attribute__((always_inline)) {
+      const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
+      va[kk][db] = __builtin_bit_cast(
+          bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      if (ks == 0) {
+        mfma_first(sn[0], ka[0], qa[0][0]);
+        mfma_first(sn[1], ka[0], qa[1][0]);
+      } else {
+        mfma_v(sn[0], ka[ks], qa[0][ks]);
+        mfma_v(sn[1], ka[ks], qa[1][ks]);
+      }
+      if (ks + 4 < kKS) ka[ks + 4] = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks + 4]));
+      else vread(0, ks - 4);
+      if ((ks & 1) == 0) dma_s(lds_u32(wdst(kdst, ks >> 1)), kg, offK[ks >> 1]);
+      // elements 2 ks, 2 ks + 1 of the order (t0 r0-7, t1 r0-7, t0 r8-15, t1 r8-15): the
+      // first key half of both tiles, which the first PV half needs
+#pragma unroll
+      for (int u = 0; u < 2; ++u) expo(ks * 2 + u);
+    }
+    bf16x8 pk[2][2];
+    auto cvt = [&](int kk) __attribute__((always_inline)) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        pk[t][kk] = kk == 0
+            ? __builtin_convertvector(__builtin_shufflevector(pr[t], pr[t], 0, 1, 2, 3, 4, 5, 6, 7), bf16x8)
+            : __builtin_convertvector(__builtin_shufflevector(pr[t], pr[t], 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+        valu_to_mfma(pk[t][kk]);
+      }
+    };
+    cvt(0);
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {  // first PV half; the second key half's exponentials
+      mfma_a(o[0][db], va[0][db], pk[0][0]);
+      mfma_a(o[1][db], va[0][db], pk[1][0]);
+      vread(1, db);
+      dma_s(lds_u32(wdst(vdst, db)), vg, offV[db]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) expo(16 + db * 4 + u);
+    }
+    cvt(1);
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+      mfma_a(o[0][db], va[1][db], pk[0][1]);
+      mfma_a(o[1][db], va[1][db], pk[1][1]);
+    }
+    // row sums of the bf16 weights (as the MFMA used them) and the range check
+    uint64_t bad = 0;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      float ls[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8 w = pk[t][kk];
+        float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, 0.0f, false);
+        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, a, false);
+        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, a, false);
+        ls[kk] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, a, false);
+      }
+      const float st = ls[0] + ls[1];
+      lsum[t] += st;
+      bad |= __builtin_amdgcn_ballot_w64(!(st <= kBig));
+    }
+    return bad;
+  };
+
+  // ---- prologue: S(0) and the reference row maxima -----------------------------------------
+  f32x16 sA[2], sB[2];
+  __syncthreads();  // every wave's part of K(0) is in LDS
+  qk(kbuf(0), sA);
+  mfma_drain();
+  if (is_special(0)) special_fix(0, sA);
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const float mt = swap_max(lane_max(sA[t])) * p.c2;
+    m[t] = mt > kInitMax ? mt : kInitMax;
+  }
+
+  // ---- steady state --------------------------------------------------------------------------
+  // Step i (i < n_it - 1): wait for this wave's loads of K(i+1), V(i) (issued two steps
+  // before; the eight loads of the previous step may still be in flight), barrier (every
+  // wave's loads landed; every wave done with step i-1), issue K(i+3) into K buffer i%3 and
+  // V(i+2) into V buffer (i+2)%3, then S(i+1) = K(i+1) Q^T, softmax of S(i), O += P V(i).
+  // Buffers depend on i mod 3 and S on i mod 2: six steps are unrolled with fixed buffers.
+  uint64_t bad = 0;
+  int i = 0;
+  const int last = n_it - 1;
+  // uniform bases of the in-loop loads: K(i+3) and V(i+2) advance one stage per step; the
+  // last (possibly ragged) stage has its own base
+  gmem_t* kg = uniform_ptr((const void*)(klb + 3 * stage_bytes));
+  gmem_t* vg = uniform_ptr((const void*)(vlb + 2 * stage_bytes));
+  gmem_t* const k_last = clean_base(klb, n_it - 1);
+  gmem_t* const v_last = clean_base(vlb, n_it - 1);
+  auto step = [&](auto ph) __attribute__((always_inline)) -> bool {
+    constexpr int P = decltype(ph)::value;
+    f32x16* sc = (P & 1) ? sB : sA;
+    f32x16* sn = (P & 1) ? sA : sB;
+    if (i == last) return true;  // finished below, outside the unrolled steps
+    if (is_special(i)) special_fix(i, sc);
+    __builtin_amdgcn_s_waitcnt(kWaitStep);
+    __builtin_amdgcn_s_barrier();
+    const int sk = clamp_stage(i + 3), sv = clamp_stage(i + 2);
+    bad |= fused(kbuf((P + 1) % 3), sn, sc, vbuf(P % 3), kbuf(P % 3), sk == i + 3 && sk != spC ? kg : k_last,
+                 vbuf((P + 2) % 3), sv == i + 2 && sv != spC ? vg : v_last);
+    kg += stage_bytes;
+    vg += stage_bytes;
+    // stages holding seeds, and the ragged last stage, are loaded again row by row (the
+    // loads of one wave complete in order, so these land after the uniform ones above)
+    if (dirty(sk) || sk == spC) patch(kbuf(P % 3), klb, kcb, offK, sk);
+    if (dirty(sv) || sv == spC) patch(vbuf((P + 2) % 3), vlb, vcb, offV, sv);
+    ++i;
+    return false;
+  };
+  for (;;) {
+    if (step(IC<0>{})) break;
+    if (step(IC<1>{})) break;
+    if (step(IC<2>{})) break;
+    if (step(IC<3>{})) break;
+    if (step(IC<4>{})) break;
+    if (step(IC<5>{})) break;
+  }
+  // last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
+  // send the tiles through memory), V in buffer last % 3
+  {
+    f32x16 sc[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) sc[t] = (last & 1) ? sB[t] : sA[t];
+    if (is_special(last)) special_fix(last, sc);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    bf16x8 pk[2][2];
+    bad |= softmax(sc, pk, m);
+    const int vb = last % 3;
+    pv(vbuf(0) + (vb == 0 ? 0 : (vb == 1 ? (int)(vbuf(1) - vbuf(0)) : (int)(vbuf(2) - vbuf(0)))), pk);
+  }
+  if (bad) atomicOr(&sbad, 1u);
+  __syncthreads();
+
+  // ---- exact pass (only if some row's scores outgrew its first-stage maximum by 2^24) ----
+  if (sbad) {
+    mfma_drain();
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      m[t] = kInitMax;
+      lsum[t] = 0.0f;
+#pragma unroll
+      for (int db = 0; db < kDB; ++db) o[t][db] = (f32x16){};
+    }
+    for (int it = 0; it < n_it; ++it) {
+      __syncthreads();
+      ld(kbuf(0), klb, kcb, offK, false, it);
+      ld(vbuf(0), vlb, vcb, offV, true, it);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      f32x16 s[2];
+      qk(kbuf(0), s);
+      mfma_drain();
+      if (is_special(it)) special_fix(it, s);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const float mt = swap_max(lane_max(s[t])) * p.c2;
+        const float mn = mt > m[t] ? mt : m[t];
+        const float alpha = __builtin_amdgcn_exp2f(m[t] - mn);
+        m[t] = mn;
+        lsum[t] *= alpha;
+#pragma unroll
+        for (int db = 0; db < kDB; ++db) o[t][db] *= alpha;
+      }
+      bf16x8 pk[2][2];
+      (void)softmax(s, pk, m);
+      pv(vbuf(0), pk);
+      mfma_drain();
+    }
+    __syncthreads();
+  }
+
+  mfma_drain();
+  // ---- merge the two key halves, add the live diagonal term, normalise, store --------------
+  // Wave w finishes tile kh of its block; its other tile goes to the partner w ^ 2 through
+  // LDS (16 KiB per wave: the stage buffers are free now), with that tile's m and row sum.
+  float* const slot_mine = (float*)(wave == 0 ? sK0 : (wave == 1 ? sK1 : (wave == 2 ? sK2 : sV0)));
+  const int pw = wave ^ 2;
+  const float* const slot_theirs = (const float*)(pw == 0 ? sK0 : (pw == 1 ? sK1 : (pw == 2 ? sK2 : sV0)));
+  const float l_tot0 = swap_add(lsum[0]), l_tot1 = swap_add(lsum[1]);
+  auto give = [&](auto tile) __attribute__((always_inline)) {
+    constexpr int T = decltype(tile)::value;  // the tile handed to the partner
+#pragma unroll
+    for (int db = 0; db < kDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; j += 4) {
+        const f32x4 v = {o[T][db][j], o[T][db][j + 1], o[T][db][j + 2], o[T][db][j + 3]};
+        *(f32x4*)(slot_mine + (db * 4 + (j >> 2)) * 256 + lane * 4) = v;
+      }
+    sML[(wave * 2 + 0) * 64 + lane] = m[T];
+    sML[(wave * 2 + 1) * 64 + lane] = T ? l_tot1 : l_tot0;
+  };
+  if (kh) give(IC<0>{}); else give(IC<1>{});
+  __syncthreads();
+  // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
+  // d = 32 db + 8 (j / 4) + 4 hl + j % 4.
+  bf16x4 outv[kDB * 4];
+  float mm_out = 0.0f, ltot_out = 1.0f;
+  auto finish = [&](auto tile) __attribute__((always_inline)) {
+    constexpr int T = decltype(tile)::value;  // the tile finished here (= kh)
+    const float td = qd_seed ? s_live * p.c2 : -INFINITY;
+    const float mb = sML[(pw * 2 + 0) * 64 + lane], lb = sML[(pw * 2 + 1) * 64 + lane];
+    const float ma = m[T], la = T ? l_tot1 : l_tot0;
+    const float mm = fmax3(ma, mb, td);
+    const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
+    const float fd = __builtin_amdgcn_exp2f(td - mm);
+    const float ltot = la * fa + lb * fb + fd;
+    const float inv = 1.0f / ltot;
+    mm_out = mm;
+    ltot_out = ltot;
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) {
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = db * 32 + g4 * 8 + hl * 4;
+        const f32x4 tv = *(const f32x4*)(slot_theirs + (db * 4 + g4) * 256 + lane * 4);
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[T][db][g4 * 4 + e] * fa + tv[e] * fb;
+        if (block_seeded) {
+          const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
+              dg + l32 * kRow + (((d0 >> 3) ^ k_swz(l32)) << 4) + (d0 & 7) * 2);
+          v[0] += fd * bf16_lo(raw[0]);
+          v[1] += fd * bf16_hi(raw[0]);
+          v[2] += fd * bf16_lo(raw[1]);
+          v[3] += fd * bf16_hi(raw[1]);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] *= inv;
+        outv[db * 4 + g4] = __builtin_convertvector(v, bf16x4);
+      }
+    }
+  };
+  if (kh) finish(IC<1>{}); else finish(IC<0>{});
+  if (p.lse && hl == 0 && qd0 + l32 < L)
+    p.lse[((int64_t)b * p.Hq + h) * L + qd0 + l32] = (mm_out + __builtin_amdgcn_logf(ltot_out)) * kLn2;
+  // Rows go out through an LDS tile (rows padded to keep 16-byte alignment and spread banks)
+  // so that each global store writes whole 256-byte rows.
+  __syncthreads();  // every wave has read its partner's slot
+  constexpr int TROW = kRow + 16;
+  static_assert(32 * TROW <= kSBytes, "the output tile fits a slot");
+  lds_t* const tile = (lds_t*)slot_mine;
+#pragma unroll
+  for (int db = 0; db < kDB; ++db)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      *(__attribute__((address_space(3))) bf16x4*)(tile + l32 * TROW + (db * 32 + g4 * 8 + hl * 4) * 2) = outv[db * 4 + g4];
+  constexpr int CPR = kRow / 16;       // 16-byte chunks per row
+  constexpr int NRD = 32 * CPR / 64;   // reads (and stores) per lane
+  __bf16* const obase = p.out + b * p.q_sb + h * p.q_sh;
+#pragma unroll
+  for (int it = 0; it < NRD; ++it) {
+    const int idx = it * 64 + lane, row = idx / CPR, ch = idx % CPR;
+    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(tile + row * TROW + ch * 16);
+    if (qd0 + row < L) *(u32x4*)(obase + (int64_t)(qd0 + row) * p.q_sl + ch * 8) = v;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream) {
+  Params4 p;
+  p.q = (const __bf16*)a.q;
+  p.kl = (const __bf16*)a.k_live;
+  p.vl = (const __bf16*)a.v_live;
+  p.kc = (const __bf16*)a.k_cache;
+  p.vc = (const __bf16*)a.v_cache;
+  p.seed_idx = a.seed_idx;
+  p.n_seed = a.n_seed;
+  p.out = (__bf16*)a.out;
+  p.lse = a.lse;
+  p.B = a.B; p.Hq = a.Hq; p.Hkv = a.Hkv; p.L = a.L; p.max_seeds = a.max_seeds;
+  p.group = a.Hq / a.Hkv;
+  p.n_qt = (a.L + kBM - 1) / kBM;
+  const int64_t nwg = (int64_t)a.B * a.Hq * p.n_qt;
+  p.xcd_slots = (nwg % 8 == 0) ? (int)(nwg / 8) : 0;
+  p.c2 = a.scale * 1.44269504088896341f;
+  p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
+  p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
+  if (nwg > 0x7fffffff || a.d != kD) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(cover_attn_w4_kernel, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

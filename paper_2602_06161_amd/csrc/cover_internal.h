@@ -61,6 +61,7 @@ struct StatsArgs {
 };
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
