@@ -34,7 +34,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = ("paper_2602_06161_amd/csrc/cover_attn.hip",)
+KERNEL_SOURCES = ("paper_2602_06161_amd/csrc/cover_attn_w4.hip",)
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_llada_hbm_traffic.md")
 
 
@@ -192,7 +192,7 @@ def main() -> int:
                    "n_seed": c.n_seeds, "Lr": a["Lr"], "parallelism": "single GPU"},
         "roofline": {
             "bound": "mfma",
-            "kernel": "cover_attn_bf16_kernel<128>",
+            "kernel": "cover_attn_w4_kernel",
             "achieved": round(attn_tflops, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",

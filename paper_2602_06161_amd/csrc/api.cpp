@@ -1,7 +1,6 @@
 // C ABI of the COVER library: host-side validation, then one kernel launch per call.
 // Every check here runs before anything is enqueued, so a rejected call writes nothing.
 #include <math.h>
-#include <stdlib.h>
 #include <stdint.h>
 
 #include "cover.h"
@@ -72,9 +71,8 @@ cover_status cover_attn_fwd(const void* q, const void* k_live, const void* v_liv
   a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
   a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
   if (D.dtype != COVER_BF16) return hip_status(cover::launch_attn_f32(a, stream));
-  static const bool w4 = getenv("COVER_DEV_ATTN4") != nullptr;  // DEVELOPMENT A/B SWITCH
-  if (D.d == 128 && w4) return hip_status(cover::launch_attn_bf16_w4(a, stream));
-  return hip_status(cover::launch_attn_bf16(a, stream));
+  if (D.d == 128) return hip_status(cover::launch_attn_bf16_w4(a, stream));
+  return hip_status(cover::launch_attn_bf16(a, stream));  // d = 64
 }
 
 cover_status cover_select_seeds(const float* logp, const float* d_in, const float* d_out,

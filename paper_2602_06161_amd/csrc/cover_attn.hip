@@ -15,7 +15,8 @@
 // removed from the P fed to the main PV product and multiplied by the live value row
 // instead.
 //
-// bf16 kernel design (one workgroup = 8 waves, two per SIMD = 128 queries of one (b, h)):
+// bf16 kernel for head size 64 (head size 128 has its own four-wave kernel, cover_attn_w4.hip);
+// design (one workgroup = 8 waves, two per SIMD = 128 queries of one (b, h)):
 //   * Transposed products keep every query row inside one lane pair:
 //       S^T = K Q^T   (v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q from registers)
 //       O^T += V^T P^T (A = V^T read with ds_read_b64_tr_b16, B = P straight from the S^T
@@ -777,11 +778,8 @@ hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream) {
   p.c2 = a.scale * 1.44269504088896341f;
   p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
   p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
-  if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-  if (a.d == 128)
-    hipLaunchKernelGGL(cover_attn_bf16_kernel<128>, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
-  else
-    hipLaunchKernelGGL(cover_attn_bf16_kernel<64>, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
+  if (nwg > 0x7fffffff || a.d != 64) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(cover_attn_bf16_kernel<64>, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 

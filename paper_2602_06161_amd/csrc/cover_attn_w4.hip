@@ -12,15 +12,19 @@
 // Layout (one workgroup = 128 queries of one (b, h); wave w: query block qb = w & 1 of 64
 // queries, key half kh = w >> 1 of every 64-key stage):
 //   * S^T = K Q^T per 32-query tile (v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q from
-//     registers) and O^T += V^T P^T (A = V^T by ds_read_b64_tr_b16, B = P from the S^T
-//     registers).  A wave owns two 32-query tiles, so every K or V^T operand read from LDS
-//     feeds two MFMAs: a stage costs the workgroup 64 KiB of LDS reads (the transposing V read
-//     delivers about a third of the bandwidth of a plain 16-byte read), not 128 KiB.
-//   * The 128 O^T accumulators per lane live in AGPRs (one wave per SIMD has 512 registers);
-//     S, P and Q stay in VGPRs.
-//   * K/V stages go global -> LDS directly (global_load_lds_dwordx4, no VGPR staging), three
-//     buffers each, issued two stages ahead of their use; each row's source (live or cache)
-//     comes from the seed bitmap, clean stages use one uniform base.
+//     AGPRs) and O^T += V^T P^T (A = V^T by ds_read_b64_tr_b16, B = P from the S^T registers).
+//     A wave owns two 32-query tiles, so every K or V^T operand read from LDS feeds two MFMAs:
+//     a stage costs the workgroup 64 KiB of LDS reads (the transposing V read delivers about a
+//     third of the bandwidth of a plain 16-byte read), not 128 KiB.
+//   * The 128 O^T accumulators per lane and Q live in AGPRs (one wave per SIMD has 512
+//     registers); S, P and the operands read from LDS stay in VGPRs.
+//   * Every global load goes straight to LDS (global_load_lds_dwordx4): the seed list, Q (read
+//     into registers once), and K/V stages in three buffers each, issued two stages ahead and
+//     spread between the MFMAs (a burst of them stalls the issuing wave on the vector-memory
+//     queue).  A stage is loaded from the live tensors through one scalar base; the rows that
+//     need another source (seed rows from the cache, rows of a ragged last stage) are loaded
+//     again one step later by exec-masked loads, only in the stages that have such rows (a
+//     scalar window of per-stage flags decides, with one scalar test per step).
 //   * Softmax without a running max: every row keeps the reference max of its first stage.
 //     A lane's per-stage probability sum above 2^24 (or not finite) flags the workgroup, which
 //     then recomputes its tile with an exact per-stage rescaling pass.  The flag never fires
@@ -50,7 +54,7 @@ typedef __attribute__((address_space(3))) char lds_t;
 typedef __attribute__((address_space(1))) const char gmem_t;
 
 constexpr int kD = 128;
-constexpr int kRow = 2 * kD;                 // bytes per K/V row
+constexpr int kRow = 2 * kD;                 // bytes per K/V/Q row
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBM = 128;                     // queries per workgroup
@@ -59,6 +63,7 @@ constexpr int kSBytes = kStage * kRow;       // one K or V stage buffer (16 KiB)
 constexpr int kLoads = kSBytes / 1024 / kWaves;  // 1-KiB loads per wave per stage buffer
 constexpr int kKS = kD / 16;                 // k-steps of S^T = K Q^T
 constexpr int kDB = kD / 32;                 // 32-row blocks of O^T
+constexpr int kSeedsLds = kThreads;          // seed positions staged in LDS (more: read directly)
 constexpr float kInitMax = -1.0e30f;         // finite "no key seen yet" reference max
 constexpr float kBig = 16777216.0f;          // 2^24
 constexpr float kLn2 = 0.693147180559945309f;
@@ -84,10 +89,10 @@ struct Params4 {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
-// LDS swizzles (64 banks of 4 bytes).  K rows: the 16-byte chunk index is XOR-ed with row % 16,
-// so the 32 rows of one b128 operand read spread over all banks.  V rows: the chunk index is
-// XOR-ed with 4 * (row % 4), so one transposing read (8 rows x 64 bytes) covers every bank
-// exactly twice.
+// LDS swizzles (64 banks of 4 bytes).  K and Q rows: the 16-byte chunk index is XOR-ed with
+// row % 16, so the 32 rows of one b128 operand read spread over all banks.  V rows: the chunk
+// index is XOR-ed with 4 * (row % 4), so one transposing read (8 rows x 64 bytes) covers every
+// bank exactly twice.
 __device__ __forceinline__ int k_swz(int row) { return row & 15; }
 __device__ __forceinline__ int v_swz(int row) { return (row & 3) << 2; }
 __device__ __forceinline__ uint32_t k_off(int row, int c) { return row * kRow + ((c ^ k_swz(row)) << 4); }
@@ -95,10 +100,11 @@ __device__ __forceinline__ uint32_t v_elem(int row, int col) {
   return row * kRow + (((col >> 3) ^ v_swz(row)) << 4) + ((col & 7) << 1);
 }
 
-// The MFMAs are written as inline assembly so that the register class of each accumulator is
-// fixed: S in VGPRs (read by the softmax), O in AGPRs (touched by VALU code only at the end).
-// The compiler does not see these as MFMAs, so the few places where VALU code reads an MFMA
-// result soon after it was written wait explicitly (mfma_drain).
+// The MFMAs are written as inline assembly so that the register class of every operand is
+// fixed: S in VGPRs (read by the softmax), O and Q in AGPRs.  The compiler does not see these
+// as MFMAs, so the few places where VALU code reads an MFMA result soon after it was written
+// wait explicitly (mfma_drain), and VALU-written operands are separated from their MFMA
+// (valu_to_mfma).
 __device__ __forceinline__ void mfma_first(f32x16& d, bf16x8 a, bf16x8 qb) {  // d = a q
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(qb));
 }
@@ -120,18 +126,41 @@ __device__ __forceinline__ u32x4 lds_read16(const lds_t* p) {
 __device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
 }
-// global -> LDS, 16 bytes per lane: lane l's bytes land at LDS byte lds + 16 l (lds uniform).
-// Inline assembly, so the compiler does not track these loads: every read of their data is
-// preceded by an explicit vmcnt wait of the issuing wave and a barrier.
+
+// Global -> LDS loads as inline assembly: lane l's bytes land at LDS byte lds + 16 l (or + 4 l
+// for the dword form); lds is wave-uniform.  Every global load of this kernel takes this path
+// (apart from seed lists longer than 256 entries), so the compiler tracks none of them: every
+// read of their data is preceded by an explicit vmcnt wait of the issuing wave and a barrier.
+__device__ __forceinline__ uint32_t lds_u32v(const lds_t* ptr) { return (uint32_t)(uintptr_t)ptr; }
 __device__ __forceinline__ uint32_t lds_u32(const lds_t* ptr) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ptr);
 }
-__device__ __forceinline__ void dma_s(uint32_t lds, gmem_t* sbase, uint32_t voff) {  // uniform base
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :: "s"(lds), "v"(voff), "s"(sbase) : "memory", "m0");
-}
-__device__ __forceinline__ void dma_v(uint32_t lds, gmem_t* addr) {  // per-lane address
+__device__ __forceinline__ void dma16(uint32_t lds, gmem_t* addr) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(lds), "v"((uint64_t)addr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma16s(uint32_t lds, gmem_t* base, uint32_t voff) {  // uniform base
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds), "v"(voff), "s"(base) : "memory", "m0");
+}
+// the uniform-base load for the lanes of `mask` only (exec is set and restored inside the
+// statement, so the compiler sees straight-line code; with an empty mask nothing moves).  The
+// three scalar moves and the nop keep the load five instructions behind any VALU write of the
+// scalar operands.
+__device__ __forceinline__ void dma16m(uint32_t lds, gmem_t* base, uint32_t voff, uint64_t mask) {
+  uint64_t save;
+  asm volatile("s_mov_b64 %0, exec\n\ts_mov_b64 exec, %1\n\ts_mov_b32 m0, %2\n\ts_nop 1\n\t"
+               "global_load_lds_dwordx4 %3, %4\n\ts_mov_b64 exec, %0"
+               : "=&s"(save) : "s"(mask), "s"(lds), "v"(voff), "s"(base) : "memory", "m0");
+}
+// lanes 16 k .. 16 k + 15 for each set bit k of a 4-bit value
+__device__ __forceinline__ uint64_t lane_quads(uint32_t n) {
+  const uint64_t m = (uint64_t)(n & 1u) | ((uint64_t)(n & 2u) << 15) | ((uint64_t)(n & 4u) << 30) |
+                     ((uint64_t)(n & 8u) << 45);
+  return (m << 16) - m;
+}
+__device__ __forceinline__ void dma4(uint32_t lds, gmem_t* addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
                :: "s"(lds), "v"((uint64_t)addr) : "memory", "m0");
 }
 __device__ __forceinline__ float swap_max(float x) {
@@ -164,17 +193,20 @@ struct IC {
 };
 
 __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params4 p) {
-  // three K and three V stage buffers; the live value rows of the seed rows' diagonals; the
-  // seed bitmap of the sequence and its per-stage summary; merge scalars; the recompute flag
+  // Three K and three V stage buffers; Q of the workgroup on its way to registers (at the end:
+  // the live key rows of the seed rows' diagonals); the seed list, the seed bitmap of the
+  // sequence and its per-stage summary; merge scalars; the recompute flag.
   __shared__ __attribute__((aligned(1024))) char sK0[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sK1[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sK2[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sV0[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sV1[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sV2[kSBytes];
-  __shared__ __attribute__((aligned(1024))) char sDiag[kWaves * 32 * kRow];
+  __shared__ __attribute__((aligned(1024))) char sQ[kBM * kRow];
   __shared__ uint32_t bits[COVER_MAX_L / 32];
   __shared__ uint32_t sdirty[COVER_MAX_L / kStage / 32];
+  __shared__ __attribute__((aligned(16))) int32_t sSeeds[kSeedsLds];
+  __shared__ __attribute__((aligned(16))) int32_t sNs[4];
   __shared__ __attribute__((aligned(16))) float sML[kWaves * 2 * 64];
   __shared__ uint32_t sbad;
   auto kbuf = [&](int n) __attribute__((always_inline)) -> lds_t* { return (lds_t*)(n == 0 ? sK0 : (n == 1 ? sK1 : sK2)); };
@@ -202,12 +234,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   const int n_it = (L + kStage - 1) / kStage;
   const int64_t sbase = (int64_t)b * p.max_seeds;
 
-  // ---- seed list first: the loads below complete in order, so its wait is short ----------
-  int ns = 0;
-  if (p.max_seeds > 0) ns = p.n_seed[b];
-  const int sj0 = tid < p.max_seeds ? p.seed_idx[sbase + tid] : -1;
-
-  // ---- stage loads ---------------------------------------------------------------------
+  // ---- load geometry -------------------------------------------------------------------
   // Load j of this wave covers stage rows (wave * 4 + j) * 4 + lane / 16, physical chunk
   // lane % 16 (logical chunk = physical ^ swizzle), landing at byte (wave * 4 + j) * 1024 +
   // 16 lane of the stage buffer, which is where the swizzled layout wants it.
@@ -229,61 +256,67 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   gmem_t* const vlb = uniform_ptr(p.vl + kvoff);
   gmem_t* const vcb = uniform_ptr(p.vc + kvoff);
   auto clamp_stage = [=](int i) __attribute__((always_inline)) -> int { return i < n_it ? i : n_it - 1; };
-  auto wdst = [&](lds_t* buf, int j) __attribute__((always_inline)) -> lds_t* { return buf + (wave * kLoads + j) * 1024; };
-  // speculative loads from the live tensors, rows past L clamped
+  auto wdst = [&](lds_t* buf, int j) __attribute__((always_inline)) -> uint32_t {
+    return lds_u32(buf + (wave * kLoads + j) * 1024);
+  };
+  // the loads of one stage from the live tensors, rows past L clamped (before the seeds are known)
   auto ld_live = [&](lds_t* buf, gmem_t* live, bool is_v, int stage) __attribute__((always_inline)) {
     const int kb = stage * kStage;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int key = min(kb + ld_row(j), L - 1);
-      dma_v(lds_u32(wdst(buf, j)), live + key * row_bytes + ld_chunk(j, is_v));
+      dma16(wdst(buf, j), live + key * row_bytes + ld_chunk(j, is_v));
     }
   };
-  // K(0); Q; V(0), K(1); V(1), K(2)
-  ld_live(kbuf(0), klb, false, 0);
 
-  // ---- Q fragments: tile t, query qw + 32 t + l32, d-chunk 2 ks + hl --------------------
-  bf16x8 qreg[2][kKS];
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int qi = min(qw + 32 * t + l32, L - 1);
-    const __bf16* qrow = qbase + (int64_t)qi * p.q_sl + hl * 8;
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) qreg[t][ks] = *(const bf16x8*)(qrow + ks * 16);
+  // ---- prologue loads, in this order: the seed count and the first 256 seed positions,
+  // K(0), Q, then V(0), K(1), V(1), K(2) --------------------------------------------------
+  if (p.max_seeds > 0) {
+    if (tid == 0) dma4(lds_u32((lds_t*)sNs), (gmem_t*)(p.n_seed + b));
+    const int e = 64 * wave + lane;
+    if (e < p.max_seeds && e < kSeedsLds)
+      dma4(lds_u32((lds_t*)sSeeds + 256 * wave), (gmem_t*)(p.seed_idx + sbase + e));
   }
-  // The live key rows of this wave's diagonal tile, loaded for every tile before the seeds
-  // are known (they are L2-resident: the same rows are K rows of this head): a seed row needs
-  // its raw live diagonal score q_i . k_live_i (lane pair halves of d, summed by a swap).
-  u32x4 klive[kKS];
-  {
-    const int qr = min(qw + 32 * kh + l32, L - 1);
-    const uint32_t* krow = (const uint32_t*)(p.kl + kvoff + (int64_t)qr * p.kv_sl + hl * 8);
+  ld_live(kbuf(0), klb, false, 0);
+  // Q rows q0 + r (r = 32 wave + 4 j + lane / 16), rows past L clamped, K swizzle
 #pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) klive[ks] = *(const u32x4*)(krow + ks * 8);
+  for (int j = 0; j < 8; ++j) {
+    const int r = 32 * wave + 4 * j + (lane >> 4), pc = lane & 15;
+    const int qi = min(q0 + r, L - 1);
+    dma16(lds_u32((lds_t*)sQ + (32 * wave + 4 * j) * kRow),
+          (gmem_t*)(qbase + (int64_t)qi * p.q_sl) + ((pc ^ k_swz(r)) << 4));
   }
   ld_live(vbuf(0), vlb, true, 0);
   ld_live(kbuf(1), klb, false, clamp_stage(1));
   ld_live(vbuf(1), vlb, true, clamp_stage(1));
   ld_live(kbuf(2), klb, false, clamp_stage(2));
-  // the seed list, K(0), Q and the live diagonal rows have landed once no more than the
-  // sixteen stage loads issued after them are outstanding
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * kLoads));
-
-
-  // ---- seed bitmap of this sequence -----------------------------------------------------
-  const int nwords = (L + 31) >> 5;
   // words past the sequence are cleared too: per-stage lookups read two words per stage
   for (int w = tid; w < 2 * n_it; w += kThreads) bits[w] = 0u;
   if (tid < COVER_MAX_L / kStage / 32) sdirty[tid] = 0u;
   if (tid == 0) sbad = 0u;
+  // the O^T accumulators start at zero (written while the loads are in flight)
+  f32x16 o[2][kDB];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int db = 0; db < kDB; ++db) asm volatile("; O = 0" : "=a"(o[t][db]) : "0"((f32x16){}));
+  // the seed list, K(0) and Q have landed once no more than the sixteen stage loads issued
+  // after them are outstanding
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * kLoads));
   __syncthreads();
+
+  // ---- seed bitmap of this sequence -----------------------------------------------------
+  int ns = p.max_seeds > 0 ? sNs[0] : 0;
   ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
   auto mark = [&](int j) __attribute__((always_inline)) {
     atomicOr(&bits[j >> 5], 1u << (j & 31));
     atomicOr(&sdirty[j >> 11], 1u << ((j >> 6) & 31));
   };
-  if (tid < ns && (unsigned)sj0 < (unsigned)L) mark(sj0);
-  for (int t = tid + kThreads; t < ns; t += kThreads) {
+  if (tid < ns && tid < kSeedsLds) {
+    const int j = sSeeds[tid];
+    if ((unsigned)j < (unsigned)L) mark(j);
+  }
+  for (int t = tid + kSeedsLds; t < ns; t += kThreads) {  // long seed lists
     const int j = p.seed_idx[sbase + t];
     if ((unsigned)j < (unsigned)L) mark(j);
   }
@@ -300,45 +333,83 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     return (w >> (stage & 31)) & 1u;
   };
   const int spC = L % kStage != 0 ? n_it - 1 : -1;  // ragged last stage
+  // stages 0..63 that need row-by-row loads (seeds, or the ragged end), as a scalar mask, so
+  // the per-step check costs no lane reads; later stages use the lane lookup
+  // The rows of a stage that this wave loads are rows 16 wave .. 16 wave + 15; their seed flags
+  // (a 16-bit chunk of the stage's 64) sit in lane `stage` of seed_chunk_l for stages below 64.
+  auto chunk_of = [&](int stage) __attribute__((always_inline)) -> uint32_t {
+    return (bits[2 * stage + (wave >> 1)] >> (16 * (wave & 1))) & 0xffffu;
+  };
+  // lane s holds the chunk of stage s (stages below 64; later ones are read from the bitmap)
+  const uint32_t seed_chunk_l = lane < n_it ? chunk_of(lane) : 0u;
+  auto seed_chunk = [&](int stage) __attribute__((always_inline)) -> uint32_t {
+    if (__builtin_expect(stage < 64, 1)) return __builtin_amdgcn_readlane(seed_chunk_l, stage);
+    return __builtin_amdgcn_readfirstlane(chunk_of(stage));
+  };
+  // Row-by-row flags of stages w0 .. w0 + 63 (w0 a multiple of 32) as one scalar: bit s - w0
+  // is set for a stage with seeds, or the ragged last one.
+  auto flags_at = [&](int w0) __attribute__((always_inline)) -> uint64_t {
+    constexpr int kWords = COVER_MAX_L / kStage / 32;
+    const int w = w0 >> 5;
+    const uint32_t a = sdirty[w];
+    const uint32_t c = w + 1 < kWords ? sdirty[w + 1] : 0u;
+    uint64_t f = ((uint64_t)__builtin_amdgcn_readfirstlane(c) << 32) | __builtin_amdgcn_readfirstlane(a);
+    if (spC >= w0 && spC < w0 + 64) f |= 1ull << (spC - w0);
+    return f;
+  };
 
-  // Issue the loads of one stage of K or V.  Stages without seeds and within L use a uniform
-  // base and per-lane 32-bit offsets; the others choose each row's source and clamp rows past L.
-  auto ld = [&](lds_t* buf, gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v,
-                int stage_in) __attribute__((always_inline)) {
-    const int stage = __builtin_amdgcn_readfirstlane(stage_in);
+  // Per-lane source addresses of the loads of one stage: the live row, or the cached row at
+  // a seed position, rows past L clamped (stages without seeds inside L: base + offset).
+  auto addrs = [&](gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v, int stage,
+                   gmem_t** a) __attribute__((always_inline)) {
     if (stage != spC && !dirty(stage)) {
       gmem_t* lb = uniform_ptr((const void*)(live + stage * stage_bytes));
 #pragma unroll
-      for (int j = 0; j < kLoads; ++j) dma_s(lds_u32(wdst(buf, j)), lb, off[j]);
+      for (int j = 0; j < kLoads; ++j) a[j] = lb + off[j];
     } else {
       const int kb = stage * kStage;
 #pragma unroll
       for (int j = 0; j < kLoads; ++j) {
         const int key = min(kb + ld_row(j), L - 1);
-        gmem_t* src = is_seed(key) ? cache : live;
-        dma_v(lds_u32(wdst(buf, j)), src + key * row_bytes + ld_chunk(j, is_v));
+        a[j] = (is_seed(key) ? cache : live) + key * row_bytes + ld_chunk(j, is_v);
       }
     }
   };
+  auto ld = [&](lds_t* buf, gmem_t* live, gmem_t* cache, const uint32_t* off, bool is_v,
+                int stage) __attribute__((always_inline)) {
+    gmem_t* a[kLoads];
+    addrs(live, cache, off, is_v, stage, a);
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) dma16(wdst(buf, j), a[j]);
+  };
 
-  // After the uniform loads of a stage (issued earlier by the same wave, so they land first),
-  // reload the rows that need another source: seed rows from the cache, and in the ragged
-  // last stage the rows below L (the uniform loads read the last 64 rows there).  Only the
-  // lanes of such rows take part.
+  // Uniform base of the in-loop loads of a stage: its rows, or for the ragged last stage the
+  // last 64 rows of the sequence (in bounds; the rows below L are then reloaded by patch).
+  auto clean_base = [&](gmem_t* live, int stage) __attribute__((always_inline)) -> gmem_t* {
+    const int64_t off = stage == spC ? (int64_t)(L - kStage) * row_bytes : stage * stage_bytes;
+    return uniform_ptr((const void*)(live + off));
+  };
+  // Reload the rows of a stage that the uniform loads got wrong: in the ragged last stage the
+  // rows below L (from the live tensor), and every seed row (from the cache).  Issued after
+  // the uniform loads of the same wave, so these land last; load j takes the lanes of rows
+  // 16 wave + 4 j + {0..3} that need it (lane / 16 selects the row), and is skipped if there
+  // are none (back-to-back global-to-LDS loads issue slowly, so only the needed ones go out).
   auto patch = [&](lds_t* buf, gmem_t* live, gmem_t* cache, const uint32_t* off, int stage_in)
                    __attribute__((always_inline)) {
     const int st = __builtin_amdgcn_readfirstlane(stage_in);
-    gmem_t* lb = uniform_ptr((const void*)(live + st * stage_bytes));
-    gmem_t* cb = uniform_ptr((const void*)(cache + st * stage_bytes));
-    const bool ragged = st == spC;
-    const uint64_t sm = ((uint64_t)bits[2 * st + 1] << 32) | bits[2 * st];  // the stage's seeds
+    if (st == spC) {
+      gmem_t* lb = uniform_ptr((const void*)(live + st * stage_bytes));
+      const int nv = min(max(L - st * kStage - 16 * wave, 0), 16);  // this wave's rows below L
+      const uint32_t vm = (1u << nv) - 1u;
 #pragma unroll
-    for (int j = 0; j < kLoads; ++j) {
-      const int r = ld_row(j);
-      const bool in = st * kStage + r < L;
-      if (ragged && in) dma_s(lds_u32(wdst(buf, j)), lb, off[j]);
-      if (in && ((sm >> r) & 1u)) dma_s(lds_u32(wdst(buf, j)), cb, off[j]);
+      for (int j = 0; j < kLoads; ++j)
+        if ((vm >> (4 * j)) & 15u) dma16m(wdst(buf, j), lb, off[j], lane_quads((vm >> (4 * j)) & 15u));
     }
+    gmem_t* cb = uniform_ptr((const void*)(cache + st * stage_bytes));
+    const uint32_t sc = seed_chunk(st);  // seeds lie below L
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j)
+      if ((sc >> (4 * j)) & 15u) dma16m(wdst(buf, j), cb, off[j], lane_quads((sc >> (4 * j)) & 15u));
   };
 
   // ---- diagonal set-up --------------------------------------------------------------------
@@ -353,64 +424,32 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   const bool block_seeded = __builtin_amdgcn_ballot_w64(qd_seed) != 0;
   const int spA = block_seeded ? sd : -1;
   auto is_special = [=](int i) __attribute__((always_inline)) -> bool { return (i == spA) | (i == spC); };
-  // uniform base of a stage's rows for the in-loop loads: the ragged last stage reads the
-  // last 64 rows instead (in bounds; it is then reloaded row by row)
-  auto clean_base = [&](gmem_t* live, int stage) __attribute__((always_inline)) -> gmem_t* {
-    const int64_t off = stage == spC ? (int64_t)(L - kStage) * row_bytes : stage * stage_bytes;
-    return uniform_ptr((const void*)(live + off));
-  };
 
   // Stages 0..2 were loaded from the live tensors before the seeds were known; reload the
-  // ones that hold seeds (after every wave's speculative loads have landed).
-  {
-    const bool redo = dirty(0) || dirty(clamp_stage(1)) || dirty(clamp_stage(2));
-    if (redo) {
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      ld(kbuf(0), klb, kcb, offK, false, 0);
-      ld(vbuf(0), vlb, vcb, offV, true, 0);
-      ld(kbuf(1), klb, kcb, offK, false, clamp_stage(1));
-      ld(vbuf(1), vlb, vcb, offV, true, clamp_stage(1));
-      ld(kbuf(2), klb, kcb, offK, false, clamp_stage(2));
-    }
-  }
-  // Seed rows of the diagonal tile: their live value rows (K swizzle) and the raw live
-  // diagonal score q_i . k_live_i (lane pair halves of d, summed by a swap).
-  lds_t* const dg = (lds_t*)sDiag + wave * (32 * kRow);
-  if (block_seeded) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int row = j * 4 + (lane >> 4), pc = lane & 15;
-      const int vr = min(qd0 + row, L - 1);
-      dma_v(lds_u32(dg + j * 1024), vlb + vr * row_bytes + ((pc ^ k_swz(row)) << 4));
-    }
-  }
-  // (computed on every path: a load left unconsumed on one path would make the compiler wait
-  // for all memory operations at the next write of its registers, inside the main loop)
-  float s_live;
-  {
-    float acc = 0.0f;
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      const u32x4 kv = klive[ks];
-      const bf16x8 q0v = qreg[0][ks], q1v = qreg[1][ks];
-      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
-        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
-      }
-    }
-    s_live = swap_add(acc);
+  // ones that hold seeds (after every wave's first loads have landed).
+  if (dirty(0) || dirty(clamp_stage(1)) || dirty(clamp_stage(2))) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __syncthreads();
+    ld(kbuf(0), klb, kcb, offK, false, 0);
+    ld(vbuf(0), vlb, vcb, offV, true, 0);
+    ld(kbuf(1), klb, kcb, offK, false, clamp_stage(1));
+    ld(vbuf(1), vlb, vcb, offV, true, clamp_stage(1));
+    ld(kbuf(2), klb, kcb, offK, false, clamp_stage(2));
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * kLoads));  // K(0) back in place
+    __syncthreads();
   }
 
-  // Q moves to AGPRs for good (the B operand of S^T = K Q^T may come from either file; the
-  // VGPRs are needed for S, P and the operands read from LDS)
+  // ---- Q fragments (B operand of S^T = K Q^T): tile t, query qw + 32 t + l32, d-chunk
+  // 2 ks + hl, from LDS into AGPRs for good -------------------------------------------------
   bf16x8 qa[2][kKS];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) asm volatile("; Q to AGPR" : "=a"(qa[t][ks]) : "0"(qreg[t][ks]));
+    for (int ks = 0; ks < kKS; ++ks) {
+      const int r = 64 * qb + 32 * t + l32;
+      asm volatile("ds_read_b128 %0, %1" : "=a"(qa[t][ks]) : "v"(lds_u32v((lds_t*)sQ + k_off(r, 2 * ks + hl))));
+    }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the Q reads above (not tracked by the compiler)
 
   // ---- per-lane LDS read addresses (relative to a stage buffer) ---------------------------
   uint32_t kaddr[kKS];
@@ -429,7 +468,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     for (int db = 0; db < kDB; ++db) vaddr[db] = v_elem(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
   }
 
-  // ---- the three compute pieces ------------------------------------------------------------
+  // ---- compute pieces ----------------------------------------------------------------------
   auto qk = [&](const lds_t* kb, f32x16* s) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
@@ -445,47 +484,38 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   };
   // keys of this wave's half of `stage` past L, and the seed rows' own (cached) column, get no
   // weight; the live diagonal term joins in the epilogue
+  // (The per-lane limits pass through an empty asm at each use: otherwise the compiler keeps
+  // the 32 element masks of each test alive across the loop as scalar register pairs.)
   auto special_fix = [&](int stage, f32x16* s) __attribute__((always_inline)) {
     if (stage * kStage + kStage > L) {
-      const int kbase = stage * kStage + kh * 32;
+      // element r holds key stage * 64 + 32 kh + 8 (r / 4) + 4 hl + r % 4
+      int lim = L - (stage * kStage + kh * 32) - 4 * hl;
+      asm volatile("" : "+v"(lim));
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool ok = kbase + ((r >> 2) << 3) + hl * 4 + (r & 3) < L;
-          s[t][r] = ok ? s[t][r] : -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r) s[t][r] = ((r >> 2) << 3) + (r & 3) < lim ? s[t][r] : -INFINITY;
     }
     if (block_seeded && stage == sd) {
       // tile kh holds the diagonal; both tiles are written with value selects only (a
       // branch per tile would make the compiler address the tiles through memory)
+      int dsel = diag_seed ? rd : -1;
+      asm volatile("" : "+v"(dsel));
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[t][r] = (kh == t && diag_seed && r == rd) ? -INFINITY : s[t][r];
+        for (int r = 0; r < 16; ++r) s[t][r] = (kh == t && r == dsel) ? -INFINITY : s[t][r];
     }
   };
 
   float m[2], lsum[2] = {0.0f, 0.0f};
-  f32x16 o[2][kDB];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int db = 0; db < kDB; ++db) o[t][db] = (f32x16){};
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // exp2(c2 s - m) -> bf16 P (both tiles), row sums of the bf16 weights as the MFMA sees them;
-  // returns the lanes whose per-stage sum left the safe range
-  auto softmax = [&](const f32x16* s, bf16x8 (*pk)[2], float* mref) __attribute__((always_inline)) -> uint64_t {
+  // row sums of the bf16 weights (as the MFMA used them) and the range check
+  auto rowsums = [&](bf16x8 (*pk)[2]) __attribute__((always_inline)) -> uint64_t {
     uint64_t bad = 0;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const float nm = -mref[t];
-      f32x16 pr;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], p.c2, nm));
-      pk[t][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
-      pk[t][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
       float ls[2];
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
@@ -500,6 +530,20 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       bad |= __builtin_amdgcn_ballot_w64(!(st <= kBig));
     }
     return bad;
+  };
+  // exp2(c2 s - m) -> bf16 P (both tiles); returns the lanes whose per-stage sum left the
+  // safe range
+  auto softmax = [&](const f32x16* s, bf16x8 (*pk)[2], float* mref) __attribute__((always_inline)) -> uint64_t {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const float nm = -mref[t];
+      f32x16 pr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][r], p.c2, nm));
+      pk[t][0] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
+      pk[t][1] = __builtin_convertvector(__builtin_shufflevector(pr, pr, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+    }
+    return rowsums(pk);
   };
   auto pv = [&](const lds_t* vb, bf16x8 (*pk)[2]) __attribute__((always_inline)) {
 #pragma unroll
@@ -519,18 +563,12 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
   };
 
-  // The main block of a step: S(i+1) = K(i+1) Q^T, softmax of S(i), O += P(i) V(i), written
-  // in issue order (the MFMAs keep their order; LDS reads stay where they are written, ahead
-  // of their use): K operands four k-steps ahead, V operands one d-block ahead; the softmax
-  // elements of the first key half of both tiles go between the S MFMAs, so that the P of
-  // the first PV half is ready when the S MFMAs end.
-  // The main block of a step: S(i+1) = K(i+1) Q^T - m, softmax of S(i), O += P(i) V(i), and
-  // the loads of K(i+3) and V(i+2), written in issue order (the MFMAs keep their order; LDS
-  // reads and global loads stay where they are written): K operands four k-steps ahead, V
-  // operands one d-block ahead, one global load between MFMA pairs (a burst of eight stalls
-  // the issuing wave on the vector-memory queue); the exponentials of the first key half of
-  // both tiles go between the S MFMAs, so that the P of the first PV half is ready when they
-  // end.
+  // The main block of a step: S(i+1) = K(i+1) Q^T, softmax of S(i), O += P(i) V(i), and the
+  // loads of K(i+3) and V(i+2), written in issue order (the MFMAs keep their order; LDS reads
+  // and global loads stay where they are written): K operands four k-steps ahead, V operands
+  // one d-block ahead, one global load between MFMA pairs; the exponentials of the first key
+  // half of both tiles go between the S MFMAs (the first PV half needs them), those of the
+  // second half between the first PV half's MFMAs.
   auto fused = [&](const lds_t* kb, f32x16* sn, const f32x16* sc, const lds_t* vb, lds_t* kdst,
                    gmem_t* kg, lds_t* vdst, gmem_t* vg) __attribute__((always_inline)) -> uint64_t {
     bf16x8 ka[kKS];
@@ -559,9 +597,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       }
       if (ks + 4 < kKS) ka[ks + 4] = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks + 4]));
       else vread(0, ks - 4);
-      if ((ks & 1) == 0) dma_s(lds_u32(wdst(kdst, ks >> 1)), kg, offK[ks >> 1]);
-      // elements 2 ks, 2 ks + 1 of the order (t0 r0-7, t1 r0-7, t0 r8-15, t1 r8-15): the
-      // first key half of both tiles, which the first PV half needs
+      if ((ks & 1) == 0) dma16s(wdst(kdst, ks >> 1), kg, offK[ks >> 1]);
+      // elements 2 ks, 2 ks + 1 of the order (t0 r0-7, t1 r0-7, t0 r8-15, t1 r8-15)
 #pragma unroll
       for (int u = 0; u < 2; ++u) expo(ks * 2 + u);
     }
@@ -577,11 +614,11 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     };
     cvt(0);
 #pragma unroll
-    for (int db = 0; db < kDB; ++db) {  // first PV half; the second key half's exponentials
+    for (int db = 0; db < kDB; ++db) {
       mfma_a(o[0][db], va[0][db], pk[0][0]);
       mfma_a(o[1][db], va[0][db], pk[1][0]);
       vread(1, db);
-      dma_s(lds_u32(wdst(vdst, db)), vg, offV[db]);
+      dma16s(wdst(vdst, db), vg, offV[db]);
 #pragma unroll
       for (int u = 0; u < 4; ++u) expo(16 + db * 4 + u);
     }
@@ -591,29 +628,11 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       mfma_a(o[0][db], va[1][db], pk[0][1]);
       mfma_a(o[1][db], va[1][db], pk[1][1]);
     }
-    // row sums of the bf16 weights (as the MFMA used them) and the range check
-    uint64_t bad = 0;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      float ls[2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 w = pk[t][kk];
-        float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 0, 1), ones, 0.0f, false);
-        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 2, 3), ones, a, false);
-        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 4, 5), ones, a, false);
-        ls[kk] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(w, w, 6, 7), ones, a, false);
-      }
-      const float st = ls[0] + ls[1];
-      lsum[t] += st;
-      bad |= __builtin_amdgcn_ballot_w64(!(st <= kBig));
-    }
-    return bad;
+    return rowsums(pk);
   };
 
-  // ---- prologue: S(0) and the reference row maxima -----------------------------------------
+  // ---- prologue compute: S(0) and the reference row maxima --------------------------------
   f32x16 sA[2], sB[2];
-  __syncthreads();  // every wave's part of K(0) is in LDS
   qk(kbuf(0), sA);
   mfma_drain();
   if (is_special(0)) special_fix(0, sA);
@@ -626,35 +645,42 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   // ---- steady state --------------------------------------------------------------------------
   // Step i (i < n_it - 1): wait for this wave's loads of K(i+1), V(i) (issued two steps
   // before; the eight loads of the previous step may still be in flight), barrier (every
-  // wave's loads landed; every wave done with step i-1), issue K(i+3) into K buffer i%3 and
-  // V(i+2) into V buffer (i+2)%3, then S(i+1) = K(i+1) Q^T, softmax of S(i), O += P V(i).
-  // Buffers depend on i mod 3 and S on i mod 2: six steps are unrolled with fixed buffers.
+  // wave's loads landed; every wave done with step i-1), then the main block, whose loads go
+  // to K buffer i%3 and V buffer (i+2)%3.  Past the end the loads repeat the last stage (they
+  // keep the per-step load count, which the waits rely on).  Buffers depend on i mod 3 and S
+  // on i mod 2: six steps are unrolled with fixed buffers.
   uint64_t bad = 0;
   int i = 0;
   const int last = n_it - 1;
-  // uniform bases of the in-loop loads: K(i+3) and V(i+2) advance one stage per step; the
-  // last (possibly ragged) stage has its own base
-  gmem_t* kg = uniform_ptr((const void*)(klb + 3 * stage_bytes));
-  gmem_t* vg = uniform_ptr((const void*)(vlb + 2 * stage_bytes));
+  // uniform bases of the in-loop loads: K(i+3) and V(i+2) advance a stage per step; the last
+  // (possibly ragged) stage has its own
+  gmem_t* kgr = uniform_ptr((const void*)(klb + 3 * stage_bytes));
+  gmem_t* vgr = uniform_ptr((const void*)(vlb + 2 * stage_bytes));
   gmem_t* const k_last = clean_base(klb, n_it - 1);
   gmem_t* const v_last = clean_base(vlb, n_it - 1);
+  uint64_t win = flags_at(0);  // the row-by-row flags of stages (i & ~31) + 0 .. 63
   auto step = [&](auto ph) __attribute__((always_inline)) -> bool {
     constexpr int P = decltype(ph)::value;
     f32x16* sc = (P & 1) ? sB : sA;
     f32x16* sn = (P & 1) ? sA : sB;
     if (i == last) return true;  // finished below, outside the unrolled steps
-    if (is_special(i)) special_fix(i, sc);
+    if (__builtin_expect((i & 31) == 0 && i > 0, 0)) win = flags_at(i);
+    if (__builtin_expect(is_special(i), 0)) special_fix(i, sc);
+    gmem_t* const kg = i + 3 < n_it - 1 ? kgr : k_last;
+    gmem_t* const vg = i + 2 < n_it - 1 ? vgr : v_last;
+    kgr += stage_bytes;
+    vgr += stage_bytes;
     __builtin_amdgcn_s_waitcnt(kWaitStep);
     __builtin_amdgcn_s_barrier();
-    const int sk = clamp_stage(i + 3), sv = clamp_stage(i + 2);
-    bad |= fused(kbuf((P + 1) % 3), sn, sc, vbuf(P % 3), kbuf(P % 3), sk == i + 3 && sk != spC ? kg : k_last,
-                 vbuf((P + 2) % 3), sv == i + 2 && sv != spC ? vg : v_last);
-    kg += stage_bytes;
-    vg += stage_bytes;
-    // stages holding seeds, and the ragged last stage, are loaded again row by row (the
-    // loads of one wave complete in order, so these land after the uniform ones above)
-    if (dirty(sk) || sk == spC) patch(kbuf(P % 3), klb, kcb, offK, sk);
-    if (dirty(sv) || sv == spC) patch(vbuf((P + 2) % 3), vlb, vcb, offV, sv);
+    // the stages loaded in the previous step, K(i+2) and V(i+1), get their seed / ragged
+    // rows now: after the wait (which would otherwise also wait for the previous step's
+    // loads), before this step's loads (so the wait at the top of the next step covers them);
+    // neither buffer is read in this step
+    if (__builtin_expect(((win >> ((i & 31) + 1)) & 3u) != 0, 0)) {
+      if (i + 2 < n_it) patch(kbuf((P + 2) % 3), klb, kcb, offK, i + 2);
+      patch(vbuf((P + 1) % 3), vlb, vcb, offV, i + 1);
+    }
+    bad |= fused(kbuf((P + 1) % 3), sn, sc, vbuf(P % 3), kbuf(P % 3), kg, vbuf((P + 2) % 3), vg);
     ++i;
     return false;
   };
@@ -666,15 +692,33 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     if (step(IC<4>{})) break;
     if (step(IC<5>{})) break;
   }
-  // last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
-  // send the tiles through memory), V in buffer last % 3
+  // Last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
+  // send the tiles through memory), V in buffer last % 3.  After the barrier the K buffers
+  // and the Q staging area are free: seed waves fetch the live key rows (into the Q area) and
+  // value rows (into K buffers 0 and 1) of their diagonal tile for the epilogue.
+  lds_t* const dk = (lds_t*)sQ + wave * (32 * kRow);
+  lds_t* const dv = (lds_t*)(wave < 2 ? sK0 : sK1) + (wave & 1) * (32 * kRow);
   {
     f32x16 sc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) sc[t] = (last & 1) ? sB[t] : sA[t];
     if (is_special(last)) special_fix(last, sc);
-    __builtin_amdgcn_s_waitcnt(0);
+    if (last >= 1 && (dirty(last) || last == spC)) {  // V(last), loaded in the step before
+      const int vb = last % 3;
+      patch(vb == 0 ? vbuf(0) : (vb == 1 ? vbuf(1) : vbuf(2)), vlb, vcb, offV, last);
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __builtin_amdgcn_s_barrier();
+    if (block_seeded) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int row = j * 4 + (lane >> 4), pc = lane & 15;
+        const int r = min(qd0 + row, L - 1);
+        const uint32_t c = (uint32_t)((pc ^ k_swz(row)) << 4);
+        dma16(lds_u32(dk + j * 1024), klb + r * row_bytes + c);
+        dma16(lds_u32(dv + j * 1024), vlb + r * row_bytes + c);
+      }
+    }
     bf16x8 pk[2][2];
     bad |= softmax(sc, pk, m);
     const int vb = last % 3;
@@ -684,6 +728,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   __syncthreads();
 
   // ---- exact pass (only if some row's scores outgrew its first-stage maximum by 2^24) ----
+  // Stage buffers K2 / V2 only (K0, K1 and the Q area hold the diagonal rows).
   if (sbad) {
     mfma_drain();
 #pragma unroll
@@ -695,12 +740,12 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
     for (int it = 0; it < n_it; ++it) {
       __syncthreads();
-      ld(kbuf(0), klb, kcb, offK, false, it);
-      ld(vbuf(0), vlb, vcb, offV, true, it);
-      __builtin_amdgcn_s_waitcnt(0);
+      ld(kbuf(2), klb, kcb, offK, false, it);
+      ld(vbuf(2), vlb, vcb, offV, true, it);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
       __syncthreads();
       f32x16 s[2];
-      qk(kbuf(0), s);
+      qk(kbuf(2), s);
       mfma_drain();
       if (is_special(it)) special_fix(it, s);
 #pragma unroll
@@ -715,7 +760,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       }
       bf16x8 pk[2][2];
       (void)softmax(s, pk, m);
-      pv(vbuf(0), pk);
+      pv(vbuf(2), pk);
       mfma_drain();
     }
     __syncthreads();
@@ -724,10 +769,10 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   mfma_drain();
   // ---- merge the two key halves, add the live diagonal term, normalise, store --------------
   // Wave w finishes tile kh of its block; its other tile goes to the partner w ^ 2 through
-  // LDS (16 KiB per wave: the stage buffers are free now), with that tile's m and row sum.
-  float* const slot_mine = (float*)(wave == 0 ? sK0 : (wave == 1 ? sK1 : (wave == 2 ? sK2 : sV0)));
+  // LDS (16 KiB per wave: buffers V0, V1, V2, K2 are free now), with that tile's m and row sum.
+  float* const slot_mine = (float*)(wave == 0 ? sV0 : (wave == 1 ? sV1 : (wave == 2 ? sV2 : sK2)));
   const int pw = wave ^ 2;
-  const float* const slot_theirs = (const float*)(pw == 0 ? sK0 : (pw == 1 ? sK1 : (pw == 2 ? sK2 : sV0)));
+  const float* const slot_theirs = (const float*)(pw == 0 ? sV0 : (pw == 1 ? sV1 : (pw == 2 ? sV2 : sK2)));
   const float l_tot0 = swap_add(lsum[0]), l_tot1 = swap_add(lsum[1]);
   auto give = [&](auto tile) __attribute__((always_inline)) {
     constexpr int T = decltype(tile)::value;  // the tile handed to the partner
@@ -742,6 +787,25 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     sML[(wave * 2 + 1) * 64 + lane] = T ? l_tot1 : l_tot0;
   };
   if (kh) give(IC<0>{}); else give(IC<1>{});
+  // the seed rows' own terms: the raw live diagonal score q_i . k_live_i of the finished
+  // tile (lane pair halves of d, summed by a swap), from the rows fetched in the last step
+  float s_live = 0.0f;
+  if (block_seeded) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // this wave's own diagonal rows
+    float acc = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const u32x4 kv = lds_read16(dk + k_off(l32, 2 * ks + hl));
+      const bf16x8 q0v = qa[0][ks], q1v = qa[1][ks];
+      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
+        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
+      }
+    }
+    s_live = swap_add(acc);
+  }
   __syncthreads();
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
   // d = 32 db + 8 (j / 4) + 4 hl + j % 4.
@@ -770,7 +834,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
         for (int e = 0; e < 4; ++e) v[e] = o[T][db][g4 * 4 + e] * fa + tv[e] * fb;
         if (block_seeded) {
           const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
-              dg + l32 * kRow + (((d0 >> 3) ^ k_swz(l32)) << 4) + (d0 & 7) * 2);
+              dv + l32 * kRow + (((d0 >> 3) ^ k_swz(l32)) << 4) + (d0 & 7) * 2);
           v[0] += fd * bf16_lo(raw[0]);
           v[1] += fd * bf16_hi(raw[0]);
           v[2] += fd * bf16_lo(raw[1]);

@@ -60,8 +60,8 @@ struct StatsArgs {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
-hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);
-hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);     // bf16, d = 64
+hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream);  // bf16, d = 128
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
