@@ -469,16 +469,21 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   }
 
   // ---- compute pieces ----------------------------------------------------------------------
-  auto qk = [&](const lds_t* kb, f32x16* s) __attribute__((always_inline)) {
+  // (operand reads `ahead` k-steps before their MFMAs; the exact pass keeps registers free)
+  auto qk = [&](const lds_t* kb, f32x16* s, auto ahead) __attribute__((always_inline)) {
+    constexpr int A = decltype(ahead)::value;
+    bf16x8 a[kKS];
+#pragma unroll
+    for (int ks = 0; ks < A; ++ks) a[ks] = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks]));
+      if (ks + A < kKS) a[ks + A] = __builtin_bit_cast(bf16x8, lds_read16(kb + kaddr[ks + A]));
       if (ks == 0) {
-        mfma_first(s[0], a, qa[0][ks]);
-        mfma_first(s[1], a, qa[1][ks]);
+        mfma_first(s[0], a[0], qa[0][ks]);
+        mfma_first(s[1], a[0], qa[1][ks]);
       } else {
-        mfma_v(s[0], a, qa[0][ks]);
-        mfma_v(s[1], a, qa[1][ks]);
+        mfma_v(s[0], a[ks], qa[0][ks]);
+        mfma_v(s[1], a[ks], qa[1][ks]);
       }
     }
   };
@@ -545,21 +550,26 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
     return rowsums(pk);
   };
-  auto pv = [&](const lds_t* vb, bf16x8 (*pk)[2]) __attribute__((always_inline)) {
+  // (V operands read `ahead` MFMA pairs before use; the exact pass keeps registers free)
+  auto pv = [&](const lds_t* vb, bf16x8 (*pk)[2], auto ahead) __attribute__((always_inline)) {
+    constexpr int A = decltype(ahead)::value;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) valu_to_mfma(pk[t][kk]);
+    bf16x8 va[2 * kDB];  // operand n: kk = n / kDB, db = n % kDB
+    auto vread = [&](int n) __attribute__((always_inline)) {
+      const lds_t* base = vb + vaddr[n % kDB] + (n / kDB) * 16 * kRow;
+      va[n] = __builtin_bit_cast(
+          bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
+    };
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int n = 0; n < A; ++n) vread(n);
 #pragma unroll
-      for (int db = 0; db < kDB; ++db) {
-        const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
-        const i16x8 v = __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, v);
-        mfma_a(o[0][db], a, pk[0][kk]);
-        mfma_a(o[1][db], a, pk[1][kk]);
-      }
+    for (int n = 0; n < 2 * kDB; ++n) {
+      if (n + A < 2 * kDB) vread(n + A);
+      mfma_a(o[0][n % kDB], va[n], pk[0][n / kDB]);
+      mfma_a(o[1][n % kDB], va[n], pk[1][n / kDB]);
     }
   };
 
@@ -633,7 +643,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
 
   // ---- prologue compute: S(0) and the reference row maxima --------------------------------
   f32x16 sA[2], sB[2];
-  qk(kbuf(0), sA);
+  qk(kbuf(0), sA, IC<4>{});
   mfma_drain();
   if (is_special(0)) special_fix(0, sA);
 #pragma unroll
@@ -658,6 +668,39 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   gmem_t* vgr = uniform_ptr((const void*)(vlb + 2 * stage_bytes));
   gmem_t* const k_last = clean_base(klb, n_it - 1);
   gmem_t* const v_last = clean_base(vlb, n_it - 1);
+  // Live key and value rows of the finished tile's queries (qd0 + l32, clamped below L), for
+  // the diagonal terms of its seed rows: loaded into registers by seeded waves at the last
+  // stage.  Lane half hl takes the d-chunks it also holds of Q (key: 2 ks + hl, 16 bytes
+  // each) and of O (value: d = 8 c + 4 hl + 0..3 for c = 0..15, 8 bytes each).
+  const int64_t diag_row = kvoff + (int64_t)min(qd0 + l32, L - 1) * p.kv_sl;
+  u32x4 dkr[kKS];
+  u32x2 dvr[kDB * 4];
+  auto load_diag_k = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) dkr[ks] = *(const u32x4*)(p.kl + diag_row + (2 * ks + hl) * 8);
+  };
+  auto load_diag_v = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < kDB * 4; ++c) dvr[c] = *(const u32x2*)(p.vl + diag_row + c * 8 + hl * 4);
+  };
+  // q_i . k_live_i for the finished tile's query of this lane pair (halves of d summed by
+  // a swap)
+  auto live_score = [&]() __attribute__((always_inline)) -> float {
+    float acc = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const u32x4 kv = dkr[ks];
+      const bf16x8 q0v = qa[0][ks], q1v = qa[1][ks];
+      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
+        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
+      }
+    }
+    return swap_add(acc);
+  };
+  float s_live = 0.0f;
   uint64_t win = flags_at(0);  // the row-by-row flags of stages (i & ~31) + 0 .. 63
   auto step = [&](auto ph) __attribute__((always_inline)) -> bool {
     constexpr int P = decltype(ph)::value;
@@ -693,42 +736,35 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     if (step(IC<5>{})) break;
   }
   // Last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
-  // send the tiles through memory), V in buffer last % 3.  After the barrier the K buffers
-  // and the Q staging area are free: seed waves fetch the live key rows (into the Q area) and
-  // value rows (into K buffers 0 and 1) of their diagonal tile for the epilogue.
-  lds_t* const dk = (lds_t*)sQ + wave * (32 * kRow);
-  lds_t* const dv = (lds_t*)(wave < 2 ? sK0 : sK1) + (wave & 1) * (32 * kRow);
+  // send the tiles through memory), V in buffer last % 3.  Seeded waves load their diagonal
+  // rows after the final wait, so the loads overlap the last softmax and PV product.
   {
     f32x16 sc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) sc[t] = (last & 1) ? sB[t] : sA[t];
     if (is_special(last)) special_fix(last, sc);
-    if (last >= 1 && (dirty(last) || last == spC)) {  // V(last), loaded in the step before
-      const int vb = last % 3;
-      patch(vb == 0 ? vbuf(0) : (vb == 1 ? vbuf(1) : vbuf(2)), vlb, vcb, offV, last);
-    }
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    __builtin_amdgcn_s_barrier();
+    // V(last) and its re-loaded rows were issued two steps and one step ago; the eight loads
+    // of the previous step (stages past the end) and the diagonal key rows issued here may stay
+    // in flight (loads complete in order).  Every load has landed before the buffers are
+    // reused after this block.
     if (block_seeded) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int row = j * 4 + (lane >> 4), pc = lane & 15;
-        const int r = min(qd0 + row, L - 1);
-        const uint32_t c = (uint32_t)((pc ^ k_swz(row)) << 4);
-        dma16(lds_u32(dk + j * 1024), klb + r * row_bytes + c);
-        dma16(lds_u32(dv + j * 1024), vlb + r * row_bytes + c);
-      }
+      load_diag_k();
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads + kKS));
+    } else {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads));
     }
+    __builtin_amdgcn_s_barrier();
     bf16x8 pk[2][2];
     bad |= softmax(sc, pk, m);
     const int vb = last % 3;
-    pv(vbuf(0) + (vb == 0 ? 0 : (vb == 1 ? (int)(vbuf(1) - vbuf(0)) : (int)(vbuf(2) - vbuf(0)))), pk);
+    pv(vbuf(0) + (vb == 0 ? 0 : (vb == 1 ? (int)(vbuf(1) - vbuf(0)) : (int)(vbuf(2) - vbuf(0)))), pk, IC<4>{});
+    if (block_seeded) s_live = live_score();  // the key rows' load overlapped the last stage
   }
   if (bad) atomicOr(&sbad, 1u);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // the loads past the end (their buffers are reused)
   __syncthreads();
 
   // ---- exact pass (only if some row's scores outgrew its first-stage maximum by 2^24) ----
-  // Stage buffers K2 / V2 only (K0, K1 and the Q area hold the diagonal rows).
   if (sbad) {
     mfma_drain();
 #pragma unroll
@@ -740,12 +776,12 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
     for (int it = 0; it < n_it; ++it) {
       __syncthreads();
-      ld(kbuf(2), klb, kcb, offK, false, it);
-      ld(vbuf(2), vlb, vcb, offV, true, it);
+      ld(kbuf(0), klb, kcb, offK, false, it);
+      ld(vbuf(0), vlb, vcb, offV, true, it);
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
       __syncthreads();
       f32x16 s[2];
-      qk(kbuf(2), s);
+      qk(kbuf(0), s, IC<0>{});
       mfma_drain();
       if (is_special(it)) special_fix(it, s);
 #pragma unroll
@@ -760,7 +796,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       }
       bf16x8 pk[2][2];
       (void)softmax(s, pk, m);
-      pv(vbuf(2), pk);
+      pv(vbuf(0), pk, IC<0>{});
       mfma_drain();
     }
     __syncthreads();
@@ -787,25 +823,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     sML[(wave * 2 + 1) * 64 + lane] = T ? l_tot1 : l_tot0;
   };
   if (kh) give(IC<0>{}); else give(IC<1>{});
-  // the seed rows' own terms: the raw live diagonal score q_i . k_live_i of the finished
-  // tile (lane pair halves of d, summed by a swap), from the rows fetched in the last step
-  float s_live = 0.0f;
-  if (block_seeded) {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // this wave's own diagonal rows
-    float acc = 0.0f;
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      const u32x4 kv = lds_read16(dk + k_off(l32, 2 * ks + hl));
-      const bf16x8 q0v = qa[0][ks], q1v = qa[1][ks];
-      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
-        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
-      }
-    }
-    s_live = swap_add(acc);
-  }
+  // the seed rows' raw live diagonal scores
+  if (block_seeded) load_diag_v();
   __syncthreads();
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
   // d = 32 db + 8 (j / 4) + 4 hl + j % 4.
@@ -832,9 +851,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
         f32x4 v;
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = o[T][db][g4 * 4 + e] * fa + tv[e] * fb;
-        if (block_seeded) {
-          const u32x2 raw = *(const __attribute__((address_space(3))) u32x2*)(
-              dv + l32 * kRow + (((d0 >> 3) ^ k_swz(l32)) << 4) + (d0 & 7) * 2);
+        if (block_seeded) {  // fd = 0 for rows that are not seeds
+          const u32x2 raw = dvr[db * 4 + g4];
           v[0] += fd * bf16_lo(raw[0]);
           v[1] += fd * bf16_hi(raw[0]);
           v[2] += fd * bf16_lo(raw[1]);
