@@ -737,7 +737,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   }
   // Last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
   // send the tiles through memory), V in buffer last % 3.  Seeded waves load their diagonal
-  // rows after the final wait, so the loads overlap the last softmax and PV product.
+  // key rows here, so the loads overlap the last softmax and PV product.
   {
     f32x16 sc[2];
 #pragma unroll
@@ -823,69 +823,82 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     sML[(wave * 2 + 1) * 64 + lane] = T ? l_tot1 : l_tot0;
   };
   if (kh) give(IC<0>{}); else give(IC<1>{});
-  // the seed rows' raw live diagonal scores
-  if (block_seeded) load_diag_v();
+  if (block_seeded) load_diag_v();  // the seed rows' live values, for the finish
   __syncthreads();
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
   // d = 32 db + 8 (j / 4) + 4 hl + j % 4.
   bf16x4 outv[kDB * 4];
   float mm_out = 0.0f, ltot_out = 1.0f;
-  auto finish = [&](auto tile) __attribute__((always_inline)) {
-    constexpr int T = decltype(tile)::value;  // the tile finished here (= kh)
+  // The partner's tile is read whole before any use, and the seed term is a separate
+  // instantiation, so no branch sits between a read and its use.
+  auto finish = [&](auto tile, auto seeded) __attribute__((always_inline)) {
+    constexpr int T = decltype(tile)::value;     // the tile finished here (= kh)
+    constexpr bool SD = decltype(seeded)::value;  // this wave's tile holds seed rows
+    f32x4 tv[kDB * 4];
+#pragma unroll
+    for (int n = 0; n < kDB * 4; ++n) tv[n] = *(const f32x4*)(slot_theirs + n * 256 + lane * 4);
     const float td = qd_seed ? s_live * p.c2 : -INFINITY;
     const float mb = sML[(pw * 2 + 0) * 64 + lane], lb = sML[(pw * 2 + 1) * 64 + lane];
     const float ma = m[T], la = T ? l_tot1 : l_tot0;
     const float mm = fmax3(ma, mb, td);
     const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
-    const float fd = __builtin_amdgcn_exp2f(td - mm);
+    const float fd = __builtin_amdgcn_exp2f(td - mm);  // 0 for rows that are not seeds
     const float ltot = la * fa + lb * fb + fd;
     const float inv = 1.0f / ltot;
     mm_out = mm;
     ltot_out = ltot;
 #pragma unroll
-    for (int db = 0; db < kDB; ++db) {
+    for (int n = 0; n < kDB * 4; ++n) {  // O^T block n / 4, rows 8 (n % 4) + 4 hl + 0..3
+      f32x4 v;
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = db * 32 + g4 * 8 + hl * 4;
-        const f32x4 tv = *(const f32x4*)(slot_theirs + (db * 4 + g4) * 256 + lane * 4);
-        f32x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = o[T][db][g4 * 4 + e] * fa + tv[e] * fb;
-        if (block_seeded) {  // fd = 0 for rows that are not seeds
-          const u32x2 raw = dvr[db * 4 + g4];
-          v[0] += fd * bf16_lo(raw[0]);
-          v[1] += fd * bf16_hi(raw[0]);
-          v[2] += fd * bf16_lo(raw[1]);
-          v[3] += fd * bf16_hi(raw[1]);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] *= inv;
-        outv[db * 4 + g4] = __builtin_convertvector(v, bf16x4);
+      for (int e = 0; e < 4; ++e) v[e] = o[T][n >> 2][(n & 3) * 4 + e] * fa + tv[n][e] * fb;
+      if constexpr (SD) {
+        const u32x2 raw = dvr[n];
+        v[0] += fd * bf16_lo(raw[0]);
+        v[1] += fd * bf16_hi(raw[0]);
+        v[2] += fd * bf16_lo(raw[1]);
+        v[3] += fd * bf16_hi(raw[1]);
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] *= inv;
+      outv[n] = __builtin_convertvector(v, bf16x4);
     }
   };
-  if (kh) finish(IC<1>{}); else finish(IC<0>{});
+  if (kh) {
+    if (block_seeded) finish(IC<1>{}, IC<1>{}); else finish(IC<1>{}, IC<0>{});
+  } else {
+    if (block_seeded) finish(IC<0>{}, IC<1>{}); else finish(IC<0>{}, IC<0>{});
+  }
   if (p.lse && hl == 0 && qd0 + l32 < L)
     p.lse[((int64_t)b * p.Hq + h) * L + qd0 + l32] = (mm_out + __builtin_amdgcn_logf(ltot_out)) * kLn2;
-  // Rows go out through an LDS tile (rows padded to keep 16-byte alignment and spread banks)
-  // so that each global store writes whole 256-byte rows.
-  __syncthreads();  // every wave has read its partner's slot
-  constexpr int TROW = kRow + 16;
-  static_assert(32 * TROW <= kSBytes, "the output tile fits a slot");
-  lds_t* const tile = (lds_t*)slot_mine;
+  // Rows go out through this wave's own 8-KiB tile in the Q area (idle since Q went to
+  // registers; 16-byte chunks XOR-swizzled by row % 16), so that each global store writes
+  // whole 256-byte rows and no other wave has to be waited for.
+  lds_t* const tile = (lds_t*)sQ + wave * (32 * kRow);
 #pragma unroll
-  for (int db = 0; db < kDB; ++db)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4)
-      *(__attribute__((address_space(3))) bf16x4*)(tile + l32 * TROW + (db * 32 + g4 * 8 + hl * 4) * 2) = outv[db * 4 + g4];
+  for (int n = 0; n < kDB * 4; ++n)
+    *(__attribute__((address_space(3))) bf16x4*)(tile + k_off(l32, n) + hl * 8) = outv[n];
   constexpr int CPR = kRow / 16;       // 16-byte chunks per row
   constexpr int NRD = 32 * CPR / 64;   // reads (and stores) per lane
   __bf16* const obase = p.out + b * p.q_sb + h * p.q_sh;
+  u32x4 ov[NRD];
 #pragma unroll
   for (int it = 0; it < NRD; ++it) {
     const int idx = it * 64 + lane, row = idx / CPR, ch = idx % CPR;
-    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(tile + row * TROW + ch * 16);
-    if (qd0 + row < L) *(u32x4*)(obase + (int64_t)(qd0 + row) * p.q_sl + ch * 8) = v;
+    ov[it] = *(const __attribute__((address_space(3))) u32x4*)(tile + k_off(row, ch));
+  }
+  if (qd0 + 32 <= L) {
+#pragma unroll
+    for (int it = 0; it < NRD; ++it) {
+      const int idx = it * 64 + lane, row = idx / CPR, ch = idx % CPR;
+      *(u32x4*)(obase + (int64_t)(qd0 + row) * p.q_sl + ch * 8) = ov[it];
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < NRD; ++it) {
+      const int idx = it * 64 + lane, row = idx / CPR, ch = idx % CPR;
+      if (qd0 + row < L) *(u32x4*)(obase + (int64_t)(qd0 + row) * p.q_sl + ch * 8) = ov[it];
+    }
   }
 }
 
