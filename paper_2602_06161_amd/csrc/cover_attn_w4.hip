@@ -216,7 +216,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qb = wave & 1;   // 64-query block
-  const int kh = wave >> 1;  // key half of every stage; also the query tile this wave finishes
+  const int kh = wave >> 1;  // key half of every stage; the wave finishes queries qw + 32 kh
   const int hl = lane >> 5, l32 = lane & 31;
 
   // ---- workgroup -> (b, h, query tile); consecutive logical tiles share an XCD ------------
@@ -413,8 +413,9 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   };
 
   // ---- diagonal set-up --------------------------------------------------------------------
-  // Query tile kh of this wave (queries qd0 + c) has its diagonal keys in stage sd, key half
-  // kh, tile row c: lane half (c / 4) % 2, register (c / 8) * 4 + c % 4.
+  // A wave's query tile t holds queries qw + 32 (t ^ kh): tile 0 is always the one it finishes
+  // (queries qd0 + c), whose diagonal keys lie in stage sd, key half kh, tile row c: lane half
+  // (c / 4) % 2, register (c / 8) * 4 + c % 4; tile 1 goes to the partner wave.
   const int qd0 = qw + 32 * kh;
   const int sd = qw / kStage;
   const bool holds_diag = hl == ((l32 >> 2) & 1);
@@ -439,14 +440,14 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     __syncthreads();
   }
 
-  // ---- Q fragments (B operand of S^T = K Q^T): tile t, query qw + 32 t + l32, d-chunk
-  // 2 ks + hl, from LDS into AGPRs for good -------------------------------------------------
+  // ---- Q fragments (B operand of S^T = K Q^T): tile t, query qw + 32 (t ^ kh) + l32,
+  // d-chunk 2 ks + hl, from LDS into AGPRs for good -----------------------------------------
   bf16x8 qa[2][kKS];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
-      const int r = 64 * qb + 32 * t + l32;
+      const int r = 64 * qb + 32 * (t ^ kh) + l32;
       asm volatile("ds_read_b128 %0, %1" : "=a"(qa[t][ks]) : "v"(lds_u32v((lds_t*)sQ + k_off(r, 2 * ks + hl))));
     }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the Q reads above (not tracked by the compiler)
@@ -501,15 +502,11 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[t][r] = ((r >> 2) << 3) + (r & 3) < lim ? s[t][r] : -INFINITY;
     }
-    if (block_seeded && stage == sd) {
-      // tile kh holds the diagonal; both tiles are written with value selects only (a
-      // branch per tile would make the compiler address the tiles through memory)
+    if (block_seeded && stage == sd) {  // tile 0 holds the diagonal
       int dsel = diag_seed ? rd : -1;
       asm volatile("" : "+v"(dsel));
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[t][r] = (kh == t && r == dsel) ? -INFINITY : s[t][r];
+      for (int r = 0; r < 16; ++r) s[0][r] = r == dsel ? -INFINITY : s[0][r];
     }
   };
 
@@ -690,8 +687,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
       const u32x4 kv = dkr[ks];
-      const bf16x8 q0v = qa[0][ks], q1v = qa[1][ks];
-      const u32x4 qv = __builtin_bit_cast(u32x4, kh ? q1v : q0v);
+      const u32x4 qv = __builtin_bit_cast(u32x4, qa[0][ks]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
@@ -804,25 +800,22 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
 
   mfma_drain();
   // ---- merge the two key halves, add the live diagonal term, normalise, store --------------
-  // Wave w finishes tile kh of its block; its other tile goes to the partner w ^ 2 through
-  // LDS (16 KiB per wave: buffers V0, V1, V2, K2 are free now), with that tile's m and row sum.
+  // Wave w finishes its tile 0; its tile 1 goes to the partner w ^ 2 (for which it is tile 0)
+  // through LDS (16 KiB per wave: buffers V0, V1, V2, K2 are free now), with that tile's m and
+  // row sum.
   float* const slot_mine = (float*)(wave == 0 ? sV0 : (wave == 1 ? sV1 : (wave == 2 ? sV2 : sK2)));
   const int pw = wave ^ 2;
   const float* const slot_theirs = (const float*)(pw == 0 ? sV0 : (pw == 1 ? sV1 : (pw == 2 ? sV2 : sK2)));
   const float l_tot0 = swap_add(lsum[0]), l_tot1 = swap_add(lsum[1]);
-  auto give = [&](auto tile) __attribute__((always_inline)) {
-    constexpr int T = decltype(tile)::value;  // the tile handed to the partner
 #pragma unroll
-    for (int db = 0; db < kDB; ++db)
+  for (int db = 0; db < kDB; ++db)
 #pragma unroll
-      for (int j = 0; j < 16; j += 4) {
-        const f32x4 v = {o[T][db][j], o[T][db][j + 1], o[T][db][j + 2], o[T][db][j + 3]};
-        *(f32x4*)(slot_mine + (db * 4 + (j >> 2)) * 256 + lane * 4) = v;
-      }
-    sML[(wave * 2 + 0) * 64 + lane] = m[T];
-    sML[(wave * 2 + 1) * 64 + lane] = T ? l_tot1 : l_tot0;
-  };
-  if (kh) give(IC<0>{}); else give(IC<1>{});
+    for (int j = 0; j < 16; j += 4) {
+      const f32x4 v = {o[1][db][j], o[1][db][j + 1], o[1][db][j + 2], o[1][db][j + 3]};
+      *(f32x4*)(slot_mine + (db * 4 + (j >> 2)) * 256 + lane * 4) = v;
+    }
+  sML[(wave * 2 + 0) * 64 + lane] = m[1];
+  sML[(wave * 2 + 1) * 64 + lane] = l_tot1;
   if (block_seeded) load_diag_v();  // the seed rows' live values, for the finish
   __syncthreads();
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
@@ -831,15 +824,15 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   float mm_out = 0.0f, ltot_out = 1.0f;
   // The partner's tile is read whole before any use, and the seed term is a separate
   // instantiation, so no branch sits between a read and its use.
-  auto finish = [&](auto tile, auto seeded) __attribute__((always_inline)) {
-    constexpr int T = decltype(tile)::value;     // the tile finished here (= kh)
+  auto finish = [&](auto seeded) __attribute__((always_inline)) {
+    constexpr int T = 0;                          // the tile finished here
     constexpr bool SD = decltype(seeded)::value;  // this wave's tile holds seed rows
     f32x4 tv[kDB * 4];
 #pragma unroll
     for (int n = 0; n < kDB * 4; ++n) tv[n] = *(const f32x4*)(slot_theirs + n * 256 + lane * 4);
     const float td = qd_seed ? s_live * p.c2 : -INFINITY;
     const float mb = sML[(pw * 2 + 0) * 64 + lane], lb = sML[(pw * 2 + 1) * 64 + lane];
-    const float ma = m[T], la = T ? l_tot1 : l_tot0;
+    const float ma = m[T], la = l_tot0;
     const float mm = fmax3(ma, mb, td);
     const float fa = __builtin_amdgcn_exp2f(ma - mm), fb = __builtin_amdgcn_exp2f(mb - mm);
     const float fd = __builtin_amdgcn_exp2f(td - mm);  // 0 for rows that are not seeds
@@ -864,11 +857,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       outv[n] = __builtin_convertvector(v, bf16x4);
     }
   };
-  if (kh) {
-    if (block_seeded) finish(IC<1>{}, IC<1>{}); else finish(IC<1>{}, IC<0>{});
-  } else {
-    if (block_seeded) finish(IC<0>{}, IC<1>{}); else finish(IC<0>{}, IC<0>{});
-  }
+  if (block_seeded) finish(IC<1>{}); else finish(IC<0>{});
   if (p.lse && hl == 0 && qd0 + l32 < L)
     p.lse[((int64_t)b * p.Hq + h) * L + qd0 + l32] = (mm_out + __builtin_amdgcn_logf(ltot_out)) * kLn2;
   // Rows go out through this wave's own 8-KiB tile in the Q area (idle since Q went to
