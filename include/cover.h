@@ -23,8 +23,10 @@
  *     the call then returns COVER_ERR_INVALID or COVER_ERR_UNSUPPORTED and writes nothing.
  *   - COVER_ERR_HIP means the HIP runtime rejected the launch.
  *   - Device-resident arguments (seed lists, seed counts, selection inputs) are not
- *     validated; their contract is stated per function.  Violations give unspecified
- *     results but never out-of-bounds memory accesses.
+ *     validated by default; their contract is stated per function.  Violations give
+ *     unspecified results but never out-of-bounds memory accesses.  With the environment
+ *     variable COVER_DEBUG=1 at the time of a call, the contract is checked on the device
+ *     first and violations are recorded (see cover_debug_status).
  *   - Outputs must not alias inputs.
  */
 #ifndef COVER_H
@@ -229,6 +231,29 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
                               const uint8_t* masked, const uint8_t* drafted,
                               float* d_in, float* d_out, float* workspace,
                               const cover_stats_desc* desc, hipStream_t stream);
+
+/*
+ * cover_debug_status -- the contract checks enabled by COVER_DEBUG=1 (a debugging aid for
+ * integrations; not for production paths).
+ *
+ * While the environment variable COVER_DEBUG is "1", every cover_attn_fwd and
+ * cover_attn_stats call first checks its seed lists, and every cover_select_seeds call its
+ * inputs on U_t, with a small kernel on the same stream; a violation sets bits of a status
+ * word kept on the current GPU:
+ */
+#define COVER_DEBUG_SEED_COUNT 1        /* some n_seed[b] outside [0, max_seeds]            */
+#define COVER_DEBUG_SEED_RANGE 2        /* a listed seed position outside [0, L)             */
+#define COVER_DEBUG_SEED_DUPLICATE 4    /* a seed position listed twice in one batch row     */
+#define COVER_DEBUG_SELECT_NONFINITE 8  /* logp, d_in or d_out not finite at a j in U_t      */
+#define COVER_DEBUG_SELECT_NEGATIVE 16  /* d_in or d_out negative at a j in U_t              */
+/*
+ * cover_debug_status copies that word of the current GPU to *status (host memory) after
+ * the work already enqueued on `stream` and, if clear != 0, resets it to 0.  Unlike every
+ * other entry point it waits for `stream` to finish before returning.  Bits accumulate
+ * across calls until cleared; the word starts at 0.  Returns COVER_ERR_INVALID for a NULL
+ * status, COVER_ERR_HIP if the copy fails.
+ */
+cover_status cover_debug_status(int32_t* status, int32_t clear, hipStream_t stream);
 
 /* Static string naming a status code. */
 const char* cover_status_str(cover_status s);

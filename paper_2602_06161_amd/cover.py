@@ -19,8 +19,11 @@ COVER_F32, COVER_BF16 = 0, 1
 COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
 
-EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_select_seeds", "cover_status_str",
-            "cover_token_stats", "cover_version")
+EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_debug_status", "cover_select_seeds",
+            "cover_status_str", "cover_token_stats", "cover_version")
+# status bits of the contract checks that COVER_DEBUG=1 enables (cover_debug_status)
+COVER_DEBUG_SEED_COUNT, COVER_DEBUG_SEED_RANGE, COVER_DEBUG_SEED_DUPLICATE = 1, 2, 4
+COVER_DEBUG_SELECT_NONFINITE, COVER_DEBUG_SELECT_NEGATIVE = 8, 16
 
 
 class CoverError(RuntimeError):
@@ -80,6 +83,8 @@ def lib():
         L.cover_status_str.restype = ctypes.c_char_p
         L.cover_version.argtypes = []
         L.cover_version.restype = ctypes.c_int32
+        L.cover_debug_status.argtypes = [ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, P]
+        L.cover_debug_status.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -90,6 +95,16 @@ def status_str(s: int) -> str:
 
 def version() -> int:
     return lib().cover_version()
+
+
+def debug_status(clear: bool = False, stream=None) -> int:
+    """The contract-violation bits recorded under COVER_DEBUG=1 on the current GPU (waits
+    for `stream`); optionally reset them."""
+    v = ctypes.c_int32(0)
+    st = lib().cover_debug_status(ctypes.byref(v), 1 if clear else 0, _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_debug_status")
+    return v.value
 
 
 def _ptr(t):

@@ -28,6 +28,11 @@ const char* cover_status_str(cover_status s) {
 
 int32_t cover_version(void) { return 100; }  // 0.1.0
 
+cover_status cover_debug_status(int32_t* status, int32_t clear, hipStream_t stream) {
+  if (!status) return COVER_ERR_INVALID;
+  return hip_status(cover::debug_status(status, clear != 0, stream));
+}
+
 cover_status cover_attn_fwd(const void* q, const void* k_live, const void* v_live,
                             const void* k_cache, const void* v_cache,
                             const int32_t* seed_idx, const int32_t* n_seed,
@@ -70,6 +75,10 @@ cover_status cover_attn_fwd(const void* q, const void* k_live, const void* v_liv
   a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
   a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
   a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  if (cover::debug_enabled()) {
+    const hipError_t e = cover::launch_check_seeds(a.seed_idx, a.n_seed, D.B, D.max_seeds, D.L, stream);
+    if (e != hipSuccess) return COVER_ERR_HIP;
+  }
   if (D.dtype != COVER_BF16) return hip_status(cover::launch_attn_f32(a, stream));
   if (D.d == 128) return hip_status(cover::launch_attn_bf16_w4(a, stream));
   return hip_status(cover::launch_attn_bf16(a, stream));  // d = 64
@@ -99,6 +108,10 @@ cover_status cover_select_seeds(const float* logp, const float* d_in, const floa
   a.logp = logp; a.d_in = d_in; a.d_out = d_out; a.flags = flags;
   a.seed_idx = seed_idx; a.n_seed = n_seed; a.score = score;
   a.B = D.B; a.Lr = D.Lr; a.max_seeds = D.max_seeds; a.pos_offset = D.pos_offset;
+  if (cover::debug_enabled()) {
+    const hipError_t e = cover::launch_check_select(logp, d_in, d_out, flags, (int64_t)D.B * D.Lr, stream);
+    if (e != hipSuccess) return COVER_ERR_HIP;
+  }
   return hip_status(cover::launch_select(a, stream));
 }
 
@@ -163,6 +176,10 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
   a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
   a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
   a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  if (cover::debug_enabled()) {
+    const hipError_t e = cover::launch_check_seeds(a.seed_idx, a.n_seed, D.B, D.max_seeds, D.L, stream);
+    if (e != hipSuccess) return COVER_ERR_HIP;
+  }
   return hip_status(cover::launch_attn_stats(a, stream));
 }
 

@@ -67,4 +67,12 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
 
+// contract checks (COVER_DEBUG=1)
+bool debug_enabled();
+hipError_t launch_check_seeds(const int32_t* seed_idx, const int32_t* n_seed, int B, int max_seeds,
+                              int L, hipStream_t stream);
+hipError_t launch_check_select(const float* logp, const float* d_in, const float* d_out,
+                               const uint8_t* flags, int64_t n, hipStream_t stream);
+hipError_t debug_status(int32_t* status, bool clear, hipStream_t stream);
+
 }  // namespace cover
