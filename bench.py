@@ -17,6 +17,10 @@ Profiling helpers (what the committed rocprofv3 summaries were made with):
                        time one producer of the selection inputs at the LLaDA-8B step shape
                        (the LM head's 256 x 126464 bf16 logits; the 256-position generated
                        block of the last layer) and print its own JSON line
+  --workload step      the full decode step of a random-init 32-layer LLaDA-8B-shaped model
+                       (torch for the rest of the model, this library for every layer's
+                       attention, the token statistics, attention masses and seed selection);
+                       prints its own JSON line with the attention share of the step
 """
 from __future__ import annotations
 
@@ -64,7 +68,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="llada", choices=["llada", "dream", "batched"])
+    ap.add_argument("--workload", default="llada", choices=["llada", "dream", "batched", "step"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", choices=["attn", "select"], default=None)
     ap.add_argument("--copy-mib", type=int, default=0)
@@ -98,6 +102,8 @@ def main() -> int:
 
     if args.kernel:
         return bench_producer(args, dev, stream)
+    if args.workload == "step":
+        return bench_full_step(args, dev, stream)
 
     a = synth.step_inputs(args.workload, seed=args.seed)
     c = a["cfg"]
@@ -300,6 +306,136 @@ def bench_producer(args, dev, stream) -> int:
                       "config": cfg, "roofline": {"bound": bound, "achieved": round(achieved, 2),
                       "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
                       "algorithmic_bytes_per_launch": nbytes}}))
+    return 0
+
+
+def bench_full_step(args, dev, stream) -> int:
+    """The full decode step of a random-init LLaDA-8B-shaped model (32 layers, hidden 4096, 32
+    heads of 128, SwiGLU FFN 12288, RMSNorm, RoPE, vocabulary 126464; B=1, L=1024 = 768 prompt +
+    256 generated, bf16): torch GEMMs and element-wise ops for the rest of the model, the COVER
+    library for every layer's attention (each layer's cache = its K/V buffer of the previous
+    step), then LM head on the generated block, token statistics, the last layer's attention
+    masses and the seed selection.  Prints its own JSON line with the attention share."""
+    import numpy as np
+    import torch
+    from paper_2602_06161_amd import cover
+
+    n_layers, H, d, hidden, ffn, vocab = 32, 32, 128, 4096, 12288, 126464
+    L, prompt, gen, n_unmasked, n_seeds, max_seeds, cap = 1024, 768, 256, 128, 16, 16, 15
+    mask_id = vocab - 1
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    w = lambda *shape: torch.randn(*shape, device=dev, dtype=torch.bfloat16, generator=g) * 0.02
+    emb, lm_head = w(vocab, hidden), w(hidden, vocab)
+    layers = [dict(wqkv=w(hidden, 3 * hidden), wo=w(hidden, hidden), wgu=w(hidden, 2 * ffn),
+                   wd=w(ffn, hidden)) for _ in range(n_layers)]
+    # per-layer K/V buffers, [L, H, d]; the previous step's buffer is this step's cache
+    kv = [[(torch.zeros(L, H, d, device=dev, dtype=torch.bfloat16),
+            torch.zeros(L, H, d, device=dev, dtype=torch.bfloat16)) for _ in range(n_layers)]
+          for _ in range(2)]
+    inv = 1.0 / (10000.0 ** (torch.arange(0, d, 2, device=dev, dtype=torch.float32) / d))
+    ang = torch.arange(L, device=dev, dtype=torch.float32)[:, None] * inv[None, :]
+    cos, sin = ang.cos()[:, None, :], ang.sin()[:, None, :]
+
+    # decoding state: the 768-token prompt, 128 of the 256 generated positions unmasked, 16
+    # seeds among those (fed as [MASK] for verification, Sec. 5.1)
+    rng = np.random.default_rng(args.seed)
+    tokens = rng.integers(0, vocab - 1, size=L)
+    unm = prompt + np.sort(rng.choice(gen, n_unmasked, replace=False))
+    seeds = np.sort(rng.choice(unm, n_seeds, replace=False))
+    masked = np.ones(gen, np.uint8)
+    masked[unm - prompt] = 0
+    inp = tokens.copy()
+    inp[prompt:][masked == 1] = mask_id
+    inp[seeds] = mask_id
+    ids = torch.from_numpy(inp).to(dev)
+    cur_tok = torch.from_numpy(tokens[prompt:].astype(np.int32)).to(dev)
+    seed_idx = torch.from_numpy(seeds.astype(np.int32))[None].to(dev)
+    n_seed = torch.tensor([n_seeds], dtype=torch.int32, device=dev)
+    masked_t = torch.from_numpy(masked)[None].to(dev)
+    flags = torch.from_numpy((1 - masked) | np.isin(np.arange(prompt, L), seeds).astype(np.uint8) * 2)
+    flags = flags.to(torch.uint8)[None].to(dev)
+
+    def rmsnorm(x):
+        xf = x.float()
+        return (xf * torch.rsqrt(xf.pow(2).mean(-1, keepdim=True) + 1e-6)).to(torch.bfloat16)
+
+    def rope(x):  # [L, H, d]
+        xf = x.float()
+        a, b = xf[..., : d // 2], xf[..., d // 2:]
+        return torch.cat((a * cos - b * sin, b * cos + a * sin), -1).to(torch.bfloat16)
+
+    as4 = lambda t: t.unsqueeze(0).permute(0, 2, 1, 3)  # [L, H, d] -> [1, H, L, d] view
+    attn_ev = []
+
+    def step(parity: int, timed: bool):
+        x = emb[ids]
+        lse = q_last = None
+        for li, ly in enumerate(layers):
+            h = rmsnorm(x)
+            qkv = (h @ ly["wqkv"]).view(L, 3, H, d)
+            q = rope(qkv[:, 0])
+            k_cur, v_cur = kv[parity][li]
+            k_prev, v_prev = kv[1 - parity][li]
+            k_cur.copy_(rope(qkv[:, 1]))
+            v_cur.copy_(qkv[:, 2])
+            o = torch.empty_like(q)
+            if timed:
+                e = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                e[0].record(stream)
+            _, lse = cover.cover_attn_fwd(as4(q), as4(k_cur), as4(v_cur), as4(k_prev), as4(v_prev),
+                                          seed_idx, n_seed, out=as4(o), stream=stream,
+                                          want_lse=li == n_layers - 1)
+            if timed:
+                e[1].record(stream)
+                attn_ev.append(e)
+            x = x + o.view(L, hidden) @ ly["wo"]
+            gu = rmsnorm(x) @ ly["wgu"]
+            x = x + (torch.nn.functional.silu(gu[:, :ffn]) * gu[:, ffn:]) @ ly["wd"]
+            q_last = q
+        logits = rmsnorm(x[prompt:]) @ lm_head                       # [256, vocab]
+        logp, conf, _ = cover.cover_token_stats(logits, cur_tok, stream=stream)
+        # draft set: the most confident masked positions above 0.9, at most 15 (Sec. 5.2)
+        cm = torch.where(masked_t[0] == 1, conf, torch.full_like(conf, -1.0))
+        top = torch.topk(cm, cap).indices
+        drafted = torch.zeros_like(masked_t)
+        drafted[0, top] = (cm[top] > 0.9).to(torch.uint8)
+        k_cur, _ = kv[parity][n_layers - 1]
+        k_prev, _ = kv[1 - parity][n_layers - 1]
+        d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx, n_seed,
+                                             lse, masked_t, drafted, prompt, stream=stream)
+        return cover.cover_select_seeds(logp[None], d_in, d_out, flags, max_seeds, prompt,
+                                        stream=stream)
+
+    for i in range(2):  # warm-up; the first fills the caches
+        step(i & 1, False)
+    torch.cuda.synchronize()
+    K = max(1, min(args.steps, 20))
+    times = []
+    for i in range(K):
+        attn_ev.clear()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        step(i & 1, True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        step_ms = e0.elapsed_time(e1)
+        attn_ms = sum(a.elapsed_time(b) for a, b in attn_ev)
+        times.append((step_ms, attn_ms))
+    times.sort()
+    step_ms, attn_ms = times[len(times) // 2]
+    flops_attn = n_layers * cover.attn_flops(1, H, L, d)
+    flops_step = flops_attn + n_layers * 2 * L * hidden * (3 * hidden + hidden + 3 * ffn) + \
+        2 * gen * hidden * vocab
+    print(json.dumps({
+        "workload": "full decode step, random-init LLaDA-8B-shaped model (32 layers, hidden 4096, "
+                    "32 heads x 128, SwiGLU 12288, vocab 126464), B=1 L=1024 (768 + 256), 16 seeds",
+        "steps": K, "step_ms": round(step_ms, 3), "attn_ms": round(attn_ms, 3),
+        "attn_share": round(attn_ms / step_ms, 4),
+        "attn_us_per_layer": round(attn_ms * 1e3 / n_layers, 3),
+        "attn_flops_share": round(flops_attn / flops_step, 4),
+        "step_tflops": round(flops_step / (step_ms * 1e-3) / 1e12, 1),
+        "dtype": "bf16", "data": "synthetic (random-init weights N(0, 0.02), random token ids)"}))
     return 0
 
 

@@ -269,8 +269,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
   };
 
-  // ---- prologue loads, in this order: the seed count and the first 256 seed positions,
-  // K(0), Q, then V(0), K(1), V(1), K(2) --------------------------------------------------
+  // ---- prologue loads: the seed count and the first 256 seed positions, K(0) and Q; after
+  // they have landed, V(0), K(1), V(1), K(2) ------------------------------------------------
   if (p.max_seeds > 0) {
     if (tid == 0) dma4(lds_u32((lds_t*)sNs), (gmem_t*)(p.n_seed + b));
     const int e = 64 * wave + lane;
@@ -286,10 +286,6 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     dma16(lds_u32((lds_t*)sQ + (32 * wave + 4 * j) * kRow),
           (gmem_t*)(qbase + (int64_t)qi * p.q_sl) + ((pc ^ k_swz(r)) << 4));
   }
-  ld_live(vbuf(0), vlb, true, 0);
-  ld_live(kbuf(1), klb, false, clamp_stage(1));
-  ld_live(vbuf(1), vlb, true, clamp_stage(1));
-  ld_live(kbuf(2), klb, false, clamp_stage(2));
   // words past the sequence are cleared too: per-stage lookups read two words per stage
   for (int w = tid; w < 2 * n_it; w += kThreads) bits[w] = 0u;
   if (tid < COVER_MAX_L / kStage / 32) sdirty[tid] = 0u;
@@ -300,10 +296,15 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int db = 0; db < kDB; ++db) asm volatile("; O = 0" : "=a"(o[t][db]) : "0"((f32x16){}));
-  // the seed list, K(0) and Q have landed once no more than the sixteen stage loads issued
-  // after them are outstanding
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * kLoads));
+  // the seed list, K(0) and Q have landed; the next stages go out only now, so that Q and
+  // K(0) do not share the vector-memory path with them at the start of the kernel (V(0) and
+  // K(1) are first needed at the top of step 0)
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
+  ld_live(vbuf(0), vlb, true, 0);
+  ld_live(kbuf(1), klb, false, clamp_stage(1));
+  ld_live(vbuf(1), vlb, true, clamp_stage(1));
+  ld_live(kbuf(2), klb, false, clamp_stage(2));
 
   // ---- seed bitmap of this sequence -----------------------------------------------------
   int ns = p.max_seeds > 0 ? sNs[0] : 0;
