@@ -14,6 +14,9 @@ Functions (each cites the passage it follows):
   select            Sec. 5.3, score / adaptive budget / exclusion / top-k
   token_stats       Sec. 5.3 u(j) and Sec. 3 confidence, from logits
   attn_stats        Sec. 5.3 d_in / d_out from the head-averaged attention
+  decode_update     Sec. 5.2 drafting with a cap and the Keep/Replace/ReMask revision rule;
+                    Sec. 3 state update; Sec. 5.3 exclusion inputs of the next selection
+                    (plain numpy here, in the order the paper states the rules)
 """
 from __future__ import annotations
 
@@ -216,3 +219,70 @@ def attn_stats(q, k_live, k_cache, seed_idx, n_seed, r0, masked, drafted, scale=
                                          _ptr(m), _ptr(dr), _ptr(d_in), _ptr(d_out))
     _check(rc)
     return d_in, d_out
+
+
+def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id, tau, cap,
+                  remask_budget, pos_offset=0):
+    """One decoding step's state update over a region of Lr positions (absolute position =
+    pos_offset + region index), for each batch row:
+
+    drafting (Sec. 5.2, Drafting): D = the masked positions (token == mask_id) whose
+      confidence exceeds tau (strictly), keeping the `cap` largest confidences when more
+      qualify (ties: smaller position first); each drafted position takes its argmax token.
+    revision (Sec. 5.2, Revision outcomes), for each previous seed i (seed_idx[b, :n_seed[b]],
+      absolute positions; entries outside the region or at masked positions are ignored):
+      Keep if argmax_i == token_i; Replace (token_i = argmax_i) if they differ and
+      conf_i > tau; otherwise ReMask (token_i = mask_id).  R = the ReMasked seeds.
+    state update (Sec. 3, State update): U_t = (U_{t-1} + D) - R.
+    counters: remask_count_i += 1 for i in R (Sec. 5.3 per-position ReMask budget).
+    next selection's flags (Sec. 5.3, exclusion): bit 0 = unmasked after the update; bit 1 =
+      i was a seed this step, or remask_count_i >= remask_budget.
+
+    Confidences compare with tau in fp32.  Returns (tokens, remask_count, flags, drafted,
+    counts) with counts[b] = (|D|, kept, replaced, remasked, masked after the update).
+    """
+    tok = np.array(tokens, dtype=np.int64, copy=True)
+    am = np.asarray(argmax, dtype=np.int64)
+    c = np.asarray(conf, dtype=np.float32)
+    cnt = np.array(remask_count, dtype=np.int64, copy=True)
+    si = np.asarray(seed_idx, dtype=np.int64).reshape(tok.shape[0], -1)
+    ns = np.asarray(n_seed, dtype=np.int64).reshape(-1)
+    t32 = np.float32(tau)
+    B, Lr = tok.shape
+    flags = np.zeros((B, Lr), np.uint8)
+    drafted = np.zeros((B, Lr), np.uint8)
+    counts = np.zeros((B, 5), np.int64)
+    for b in range(B):
+        # the previous step's seeds, as region indices (each counted once)
+        seeds = set()
+        for t in range(max(0, min(int(ns[b]), si.shape[1]))):
+            i = int(si[b, t]) - pos_offset
+            if 0 <= i < Lr and tok[b, i] != mask_id:
+                seeds.add(i)
+        # drafting over M_{t-1}
+        cand = [i for i in range(Lr) if tok[b, i] == mask_id and c[b, i] > t32]
+        cand.sort(key=lambda i: (-float(c[b, i]), i))
+        D = cand[:max(0, int(cap))]
+        # revision of the seeds
+        kept = replaced = 0
+        R = []
+        for i in sorted(seeds):
+            if am[b, i] == tok[b, i]:
+                kept += 1
+            elif c[b, i] > t32:
+                replaced += 1
+                tok[b, i] = am[b, i]
+            else:
+                R.append(i)
+        # state update
+        for i in D:
+            tok[b, i] = am[b, i]
+            drafted[b, i] = 1
+        for i in R:
+            tok[b, i] = mask_id
+            cnt[b, i] += 1
+        for i in range(Lr):
+            excl = i in seeds or cnt[b, i] >= remask_budget
+            flags[b, i] = (1 if tok[b, i] != mask_id else 0) | (2 if excl else 0)
+        counts[b] = (len(D), kept, replaced, len(R), int(np.sum(tok[b] == mask_id)))
+    return tok.astype(np.int32), cnt.astype(np.int32), flags, drafted, counts.astype(np.int32)
