@@ -314,8 +314,8 @@ def bench_full_step(args, dev, stream) -> int:
     heads of 128, SwiGLU FFN 12288, RMSNorm, RoPE, vocabulary 126464; B=1, L=1024 = 768 prompt +
     256 generated, bf16): torch GEMMs and element-wise ops for the rest of the model, the COVER
     library for every layer's attention (each layer's cache = its K/V buffer of the previous
-    step), then LM head on the generated block, token statistics, the last layer's attention
-    masses and the seed selection.  Prints its own JSON line with the attention share."""
+    step), then LM head on the generated block, token statistics, the decoding-state update
+    (drafting, revision, flags), the last layer's attention masses and the seed selection.  Prints its own JSON line with the attention share."""
     import numpy as np
     import torch
     from paper_2602_06161_amd import cover
@@ -349,12 +349,13 @@ def bench_full_step(args, dev, stream) -> int:
     inp[prompt:][masked == 1] = mask_id
     inp[seeds] = mask_id
     ids = torch.from_numpy(inp).to(dev)
-    cur_tok = torch.from_numpy(tokens[prompt:].astype(np.int32)).to(dev)
+    # the region's state before the step (each timed step starts from it again)
+    tok0 = torch.from_numpy(np.where(masked == 1, mask_id, tokens[prompt:]).astype(np.int32))
+    tok0 = tok0[None].to(dev)
+    cnt0 = torch.zeros((1, gen), dtype=torch.int32, device=dev)
     seed_idx = torch.from_numpy(seeds.astype(np.int32))[None].to(dev)
     n_seed = torch.tensor([n_seeds], dtype=torch.int32, device=dev)
     masked_t = torch.from_numpy(masked)[None].to(dev)
-    flags = torch.from_numpy((1 - masked) | np.isin(np.arange(prompt, L), seeds).astype(np.uint8) * 2)
-    flags = flags.to(torch.uint8)[None].to(dev)
 
     def rmsnorm(x):
         xf = x.float()
@@ -394,12 +395,15 @@ def bench_full_step(args, dev, stream) -> int:
             x = x + (torch.nn.functional.silu(gu[:, :ffn]) * gu[:, ffn:]) @ ly["wd"]
             q_last = q
         logits = rmsnorm(x[prompt:]) @ lm_head                       # [256, vocab]
-        logp, conf, _ = cover.cover_token_stats(logits, cur_tok, stream=stream)
-        # draft set: the most confident masked positions above 0.9, at most 15 (Sec. 5.2)
-        cm = torch.where(masked_t[0] == 1, conf, torch.full_like(conf, -1.0))
-        top = torch.topk(cm, cap).indices
-        drafted = torch.zeros_like(masked_t)
-        drafted[0, top] = (cm[top] > 0.9).to(torch.uint8)
+        _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
+        # drafting (at most 15 above 0.9), revision of the seeds, state update, flags
+        tok_state, cnt_state = tok0.clone(), cnt0.clone()
+        flags, drafted, _ = cover.cover_decode_update(tok_state, am[None], conf[None], seed_idx,
+                                                      n_seed, cnt_state, mask_id, 0.9, cap, 2,
+                                                      prompt, stream=stream)
+        # u(j) of the tokens now in place (Sec. 5.3)
+        logp, _, _ = cover.cover_token_stats(logits, tok_state[0], want_conf=False,
+                                             want_argmax=False, stream=stream)
         k_cur, _ = kv[parity][n_layers - 1]
         k_prev, _ = kv[1 - parity][n_layers - 1]
         d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx, n_seed,

@@ -233,6 +233,55 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
                               const cover_stats_desc* desc, hipStream_t stream);
 
 /*
+ * Decoding-state update description.
+ *   B              batch rows (>= 0; 0 is a no-op)
+ *   Lr             region length per row (>= 0, <= COVER_MAX_LR)
+ *   max_seeds      row stride / capacity of seed_idx (>= 0)
+ *   pos_offset     absolute position of region index 0 (seed_idx holds absolute positions)
+ *   mask_id        the [MASK] token id
+ *   draft_cap      most positions drafted per row and step (>= 0)
+ *   remask_budget  ReMasks after which a position is no longer selectable as a seed
+ *   tau            confidence threshold (not NaN), used for drafting and for Replace
+ */
+typedef struct {
+  int32_t B, Lr;
+  int32_t max_seeds;
+  int32_t pos_offset;
+  int32_t mask_id;
+  int32_t draft_cap;
+  int32_t remask_budget;
+  float tau;
+} cover_update_desc;
+
+/*
+ * cover_decode_update -- one step's update of the decoding state (Sec. 5.2 drafting and
+ * revision outcomes, Sec. 3 state update, Sec. 5.3 ReMask budget and exclusion), per row:
+ *   drafting   D = the masked positions (tokens == mask_id) with conf > tau, compared in
+ *              fp32; if more than draft_cap qualify, the draft_cap largest by (conf
+ *              descending, position ascending).  Each takes its argmax token.
+ *   revision   each previous seed i (seed_idx[b, :n_seed[b]] - pos_offset; entries outside
+ *              [0, Lr) or at masked positions are ignored, repeats count once):
+ *              Keep if argmax_i == tokens_i; else Replace (tokens_i = argmax_i) if
+ *              conf_i > tau; else ReMask (tokens_i = mask_id, remask_count_i += 1).
+ *   flags      bit 0 = unmasked after the update; bit 1 = i was a seed, or
+ *              remask_count_i >= remask_budget -- the flags cover_select_seeds takes next.
+ * Arguments (all device memory, row-major [B,Lr] unless stated):
+ *   tokens int32 (in/out; the state U/M of the region), argmax int32 and conf fp32 (the
+ *   step's argmax token and its probability, e.g. from cover_token_stats), seed_idx int32
+ *   [B,max_seeds] and n_seed int32 [B] (the seeds of the step, as cover_select_seeds
+ *   emits them; may be NULL when max_seeds == 0), remask_count int32 (in/out),
+ *   flags uint8 (out, may be NULL), drafted uint8 (out, 1 = drafted this step, may be NULL),
+ *   counts int32 [B,5] (out, may be NULL): |D|, kept, replaced, remasked, masked after.
+ * One kernel launch on `stream`; every result is an exact function of the inputs.  n_seed
+ * values outside [0, max_seeds] are clamped.
+ */
+cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const float* conf,
+                                 const int32_t* seed_idx, const int32_t* n_seed,
+                                 int32_t* remask_count, uint8_t* flags, uint8_t* drafted,
+                                 int32_t* counts, const cover_update_desc* desc,
+                                 hipStream_t stream);
+
+/*
  * cover_debug_status -- the contract checks enabled by COVER_DEBUG=1 (a debugging aid for
  * integrations; not for production paths).
  *

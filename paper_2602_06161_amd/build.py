@@ -34,6 +34,7 @@ SOURCES = {
     "cover_attn.hip": [],
     "cover_attn_w4.hip": [],
     "cover_debug.hip": [],
+    "cover_decode.hip": [],
     "cover_select.hip": ["-ffp-contract=off"],  # the selection is bit-exact fp64
     "cover_stats.hip": [],
 }

@@ -19,8 +19,8 @@ COVER_F32, COVER_BF16 = 0, 1
 COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
 
-EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_debug_status", "cover_select_seeds",
-            "cover_status_str", "cover_token_stats", "cover_version")
+EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_debug_status", "cover_decode_update",
+            "cover_select_seeds", "cover_status_str", "cover_token_stats", "cover_version")
 # status bits of the contract checks that COVER_DEBUG=1 enables (cover_debug_status)
 COVER_DEBUG_SEED_COUNT, COVER_DEBUG_SEED_RANGE, COVER_DEBUG_SEED_DUPLICATE = 1, 2, 4
 COVER_DEBUG_SELECT_NONFINITE, COVER_DEBUG_SELECT_NEGATIVE = 8, 16
@@ -50,6 +50,13 @@ class TokenDesc(ctypes.Structure):
                 ("row_stride", ctypes.c_int64)]
 
 
+class UpdateDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("Lr", ctypes.c_int32), ("max_seeds", ctypes.c_int32),
+                ("pos_offset", ctypes.c_int32), ("mask_id", ctypes.c_int32),
+                ("draft_cap", ctypes.c_int32), ("remask_budget", ctypes.c_int32),
+                ("tau", ctypes.c_float)]
+
+
 class StatsDesc(ctypes.Structure):
     _fields_ = [("attn", AttnDesc), ("r0", ctypes.c_int32), ("Lr", ctypes.c_int32)]
 
@@ -76,6 +83,8 @@ def lib():
         L.cover_select_seeds.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(SelectDesc), P]
         L.cover_select_seeds.restype = ctypes.c_int
         L.cover_token_stats.argtypes = [P, P, P, P, P, ctypes.POINTER(TokenDesc), P]
+        L.cover_decode_update.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.POINTER(UpdateDesc), P]
+        L.cover_decode_update.restype = ctypes.c_int
         L.cover_token_stats.restype = ctypes.c_int
         L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
         L.cover_attn_stats.restype = ctypes.c_int
@@ -184,6 +193,46 @@ def cover_select_seeds(logp, d_in, d_out, flags, max_seeds: int, pos_offset: int
     if st != COVER_OK:
         raise CoverError(st, "cover_select_seeds")
     return seed_idx, n_seed, score
+
+
+def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id: int,
+                        tau: float, draft_cap: int, remask_budget: int, pos_offset: int = 0,
+                        flags=None, drafted=None, counts=None, want_outputs: bool = True,
+                        stream=None):
+    """One step's decoding-state update, in place on tokens and remask_count (int32 [B,Lr]);
+    argmax int32 / conf fp32 [B,Lr]; seed_idx int32 [B,max_seeds], n_seed int32 [B] (may be
+    None: no seeds).  Returns (flags uint8, drafted uint8, counts int32 [B,5]), allocated
+    unless given (None when want_outputs is False)."""
+    B, Lr = tokens.shape
+    for t, dt in ((tokens, torch.int32), (argmax, torch.int32), (conf, torch.float32),
+                  (remask_count, torch.int32)):
+        if t.shape != (B, Lr) or t.dtype != dt or not t.is_contiguous():
+            raise ValueError("update inputs must be contiguous [B,Lr] (int32 x3, fp32 conf)")
+    max_seeds = 0
+    if seed_idx is not None:
+        if seed_idx.dim() != 2 or seed_idx.shape[0] != B or seed_idx.dtype != torch.int32 or \
+                not seed_idx.is_contiguous() or n_seed is None or n_seed.shape != (B,) or \
+                n_seed.dtype != torch.int32:
+            raise ValueError("seed_idx must be contiguous int32 [B,max_seeds], n_seed int32 [B]")
+        max_seeds = seed_idx.shape[1]
+    dev = tokens.device
+    if want_outputs:
+        flags = torch.empty((B, Lr), device=dev, dtype=torch.uint8) if flags is None else flags
+        drafted = torch.empty((B, Lr), device=dev, dtype=torch.uint8) if drafted is None else drafted
+        counts = torch.empty((B, 5), device=dev, dtype=torch.int32) if counts is None else counts
+    for t, shape, dt in ((flags, (B, Lr), torch.uint8), (drafted, (B, Lr), torch.uint8),
+                         (counts, (B, 5), torch.int32)):
+        if t is not None and (t.shape != shape or t.dtype != dt or not t.is_contiguous()):
+            raise ValueError("flags/drafted must be contiguous uint8 [B,Lr], counts int32 [B,5]")
+    desc = UpdateDesc(B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget, tau)
+    st = lib().cover_decode_update(_ptr(tokens), _ptr(argmax), _ptr(conf),
+                                   _ptr(seed_idx) if max_seeds else None,
+                                   _ptr(n_seed) if max_seeds else None, _ptr(remask_count),
+                                   _ptr(flags), _ptr(drafted), _ptr(counts), ctypes.byref(desc),
+                                   _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_decode_update")
+    return flags, drafted, counts
 
 
 def cover_token_stats(logits, tokens=None, want_logp: bool = True, want_conf: bool = True,

@@ -1,0 +1,224 @@
+// COVER decoding-state update of one step on gfx950 (arXiv 2602.06161, Sec. 5.2 drafting and
+// revision, Sec. 3 state update, Sec. 5.3 ReMask budget and exclusion flags).
+//
+// One workgroup per batch row, every region position owned by one thread (positions
+// tid + m * nthreads, m < per), so all reads and writes are coalesced and the per-position
+// work needs no synchronisation.  The steps:
+//   1. the previous seeds become a bitmap of the region in LDS (entries outside the region or
+//      at masked positions are dropped, repeats collapse);
+//   2. the draft candidates (masked, confidence > tau in fp32) get a 64-bit key: the
+//      confidence mapped to an order-preserving unsigned integer in the high half, the
+//      bitwise complement of the position in the low half.  Keys are distinct and their
+//      order is (confidence descending, position ascending);
+//   3. if more candidates qualify than the cap allows, the cap-th largest key is found by a
+//      most-significant-digit radix select (8-bit digits, LDS histogram, one wave scans the
+//      256 bins), which stops at the first digit whose bucket is taken whole; the drafts are
+//      the keys at or above the prefix found;
+//   4. per position: drafting, revision of the seeds, ReMask counters, the next selection's
+//      flags, and the row's counts reduced through LDS.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace cover {
+namespace {
+
+constexpr int kMaxThreads = 1024;
+constexpr int kMaxPer = COVER_MAX_LR / kMaxThreads;
+
+struct UpdParams {
+  int32_t* tokens;
+  const int32_t* argmax;
+  const float* conf;
+  const int32_t* seed_idx;
+  const int32_t* n_seed;
+  int32_t* remask_count;
+  uint8_t* flags;
+  uint8_t* drafted;
+  int32_t* counts;
+  int Lr, per, max_seeds, pos_offset, mask_id, cap, budget;
+  float tau;
+};
+
+// fp32 -> unsigned integer with the same order over all non-NaN values (-0 taken as +0)
+__device__ __forceinline__ uint32_t ordered(float c) {
+  uint32_t u = __float_as_uint(c);
+  if (c == 0.0f) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdParams p) {
+  __shared__ uint32_t seedbits[COVER_MAX_LR / 32];
+  __shared__ uint32_t hist[256];
+  __shared__ int sums[6];  // candidates, |D|, kept, replaced, remasked, masked after
+  __shared__ uint64_t s_prefix;
+  __shared__ int s_need, s_done, s_shift;
+
+  const int b = blockIdx.x, tid = threadIdx.x, nth = blockDim.x, lane = tid & 63;
+  const int64_t base = (int64_t)b * p.Lr;
+  for (int w = tid; w < (p.Lr + 31) / 32; w += nth) seedbits[w] = 0u;
+  if (tid < 6) sums[tid] = 0;
+  __syncthreads();
+
+  // 1. seed bitmap (reads the tokens before any thread writes them)
+  int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
+  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+  for (int t = tid; t < ns; t += nth) {
+    const int64_t i = (int64_t)p.seed_idx[(int64_t)b * p.max_seeds + t] - p.pos_offset;
+    if (i >= 0 && i < p.Lr && p.tokens[base + i] != p.mask_id)
+      atomicOr(&seedbits[i >> 5], 1u << (i & 31));
+  }
+
+  // 2. candidate keys
+  int tok[kMaxPer];
+  float cf[kMaxPer];
+  uint64_t key[kMaxPer];
+  uint32_t cand = 0;
+#pragma unroll
+  for (int m = 0; m < kMaxPer; ++m) {
+    const int j = tid + m * nth;
+    tok[m] = 0;
+    cf[m] = 0.0f;
+    key[m] = 0;
+    if (m < p.per && j < p.Lr) {
+      tok[m] = p.tokens[base + j];
+      cf[m] = p.conf[base + j];
+      if (tok[m] == p.mask_id && cf[m] > p.tau) {
+        cand |= 1u << m;
+        key[m] = ((uint64_t)ordered(cf[m]) << 32) | (uint32_t)~(uint32_t)j;
+      }
+    }
+  }
+  const int nc = wave_sum(__builtin_popcount(cand));
+  if (lane == 0 && nc) atomicAdd(&sums[0], nc);
+  __syncthreads();
+
+  // 3. drafts: every candidate, or the cap largest keys
+  uint64_t keep_mask = 0, prefix = 0;  // drafted <=> candidate and (key & keep_mask) >= prefix
+  bool none = p.cap <= 0;
+  if (!none && sums[0] > p.cap) {
+    if (tid == 0) {
+      s_prefix = 0;
+      s_need = p.cap;  // rank, from the top, of the key still to be located
+      s_done = 0;
+    }
+    for (int shift = 56; shift >= 0; shift -= 8) {
+      for (int d = tid; d < 256; d += nth) hist[d] = 0u;
+      __syncthreads();
+      const uint64_t hi = shift == 56 ? 0ull : (~0ull << (shift + 8));
+      const uint64_t pre = s_prefix;
+#pragma unroll
+      for (int m = 0; m < kMaxPer; ++m)
+        if (((cand >> m) & 1u) && (key[m] & hi) == pre)
+          atomicAdd(&hist[(uint32_t)(key[m] >> shift) & 255u], 1u);
+      __syncthreads();
+      if (tid < 64) {
+        // lane l holds digits 255-4l .. 252-4l (descending); inclusive scan over the lanes
+        uint32_t h[4], s = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s += (h[q] = hist[255 - (lane * 4 + q)]);
+        uint32_t incl = s;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t v = __shfl_up(incl, o);
+          if (lane >= o) incl += v;
+        }
+        const uint32_t need = (uint32_t)s_need;
+        const uint64_t hit = __ballot(incl >= need);
+        if (lane == __builtin_ctzll(hit)) {
+          uint32_t acc = incl - s;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (acc + h[q] >= need) {
+              const uint32_t digit = 255u - (uint32_t)(lane * 4 + q);
+              s_prefix = pre | ((uint64_t)digit << shift);
+              s_need = (int)(need - acc);
+              s_shift = shift;
+              s_done = (need - acc == h[q]) ? 1 : 0;  // the whole bucket is drafted
+              break;
+            }
+            acc += h[q];
+          }
+        }
+      }
+      __syncthreads();
+      if (s_done) break;
+    }
+    prefix = s_prefix;
+    keep_mask = ~0ull << s_shift;
+  }
+
+  // 4. per-position update
+  int n_d = 0, n_keep = 0, n_rep = 0, n_rm = 0, n_masked = 0;
+#pragma unroll
+  for (int m = 0; m < kMaxPer; ++m) {
+    const int j = tid + m * nth;
+    if (m < p.per && j < p.Lr) {
+      const int64_t e = base + j;
+      const bool dr = !none && ((cand >> m) & 1u) && (key[m] & keep_mask) >= prefix;
+      const bool seed = (seedbits[j >> 5] >> (j & 31)) & 1u;
+      int t = tok[m];
+      int cnt = p.remask_count[e];
+      if (dr || seed) {
+        const int a = p.argmax[e];
+        if (dr) {
+          t = a;
+          ++n_d;
+        } else if (a == t) {
+          ++n_keep;
+        } else if (cf[m] > p.tau) {
+          t = a;
+          ++n_rep;
+        } else {
+          t = p.mask_id;
+          ++cnt;
+          ++n_rm;
+          p.remask_count[e] = cnt;
+        }
+        if (t != tok[m]) p.tokens[e] = t;
+      }
+      const bool unmasked = t != p.mask_id;
+      n_masked += unmasked ? 0 : 1;
+      if (p.flags) p.flags[e] = (uint8_t)((unmasked ? 1 : 0) | ((seed || cnt >= p.budget) ? 2 : 0));
+      if (p.drafted) p.drafted[e] = dr ? 1 : 0;
+    }
+  }
+  if (p.counts) {
+    const int v[5] = {n_d, n_keep, n_rep, n_rm, n_masked};
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const int s = wave_sum(v[k]);
+      if (lane == 0 && s) atomicAdd(&sums[1 + k], s);
+    }
+    __syncthreads();
+    if (tid < 5) p.counts[(int64_t)b * 5 + tid] = sums[1 + tid];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream) {
+  UpdParams p;
+  p.tokens = a.tokens; p.argmax = a.argmax; p.conf = a.conf;
+  p.seed_idx = a.seed_idx; p.n_seed = a.n_seed; p.remask_count = a.remask_count;
+  p.flags = a.flags; p.drafted = a.drafted; p.counts = a.counts;
+  p.Lr = a.Lr; p.max_seeds = a.max_seeds; p.pos_offset = a.pos_offset; p.mask_id = a.mask_id;
+  p.cap = a.draft_cap; p.budget = a.remask_budget; p.tau = a.tau;
+  int nth = ((a.Lr + 63) / 64) * 64;
+  if (nth < 64) nth = 64;
+  if (nth > kMaxThreads) nth = kMaxThreads;
+  p.per = (a.Lr + nth - 1) / nth;
+  if (p.per > kMaxPer) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(cover_update_kernel, dim3((unsigned)a.B), dim3((unsigned)nth), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

@@ -60,12 +60,27 @@ struct StatsArgs {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
+struct UpdateArgs {
+  int32_t* tokens;
+  const int32_t* argmax;
+  const float* conf;
+  const int32_t* seed_idx;  // may be null when max_seeds == 0
+  const int32_t* n_seed;    // may be null when max_seeds == 0
+  int32_t* remask_count;
+  uint8_t* flags;    // may be null
+  uint8_t* drafted;  // may be null
+  int32_t* counts;   // may be null
+  int32_t B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget;
+  float tau;
+};
+
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);     // bf16, d = 64
 hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream);  // bf16, d = 128
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
+hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream);
 
 // contract checks (COVER_DEBUG=1)
 bool debug_enabled();

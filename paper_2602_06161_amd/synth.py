@@ -203,3 +203,39 @@ def stats_inputs(cfg: AttnConfig | str = "llada", seed: int = 0, n_draft: int = 
     a.update(masked=torch.from_numpy(masked), drafted=torch.from_numpy(drafted), r0=c.prompt,
              Lr=Lr)
     return a
+
+
+def update_inputs(B: int, Lr: int, seed: int = 0, vocab: int = 126464, masked_frac: float = 0.5,
+                  n_seeds: int = 16, max_seeds: int = 16, conf_levels: int = 0,
+                  keep_frac: float = 0.4, pos_offset: int = 768) -> dict:
+    """Host tensors for one decoding-state update over a region of Lr positions per row:
+    tokens with about masked_frac at mask_id (= vocab - 1), the step's argmax tokens (equal to
+    the current token at about keep_frac of the unmasked positions), confidences (uniform on
+    [0, 1) in fp32, or drawn from conf_levels distinct values when conf_levels > 0, which
+    makes ties), seeds = min(n_seeds, #unmasked) distinct unmasked positions per row (absolute
+    positions, region start pos_offset, listed in random order, then -1), ReMask counters in
+    [0, 3]."""
+    rng = np.random.default_rng(seed)
+    mask_id = vocab - 1
+    tokens = rng.integers(0, vocab - 1, (B, Lr))
+    tokens[rng.random((B, Lr)) < masked_frac] = mask_id
+    argmax = rng.integers(0, vocab - 1, (B, Lr))
+    same = (rng.random((B, Lr)) < keep_frac) & (tokens != mask_id)
+    argmax[same] = tokens[same]
+    if conf_levels > 0:
+        conf = rng.choice(rng.random(conf_levels), (B, Lr))
+    else:
+        conf = rng.random((B, Lr))
+    seed_idx = np.full((B, max(max_seeds, 0)), -1, np.int64)
+    n_seed = np.zeros(B, np.int64)
+    for b in range(B):
+        um = np.nonzero(tokens[b] != mask_id)[0]
+        k = min(n_seeds, um.size, max_seeds)
+        seed_idx[b, :k] = pos_offset + rng.choice(um, k, replace=False)
+        n_seed[b] = k
+    t = lambda x, dt: torch.from_numpy(np.ascontiguousarray(x)).to(dt)
+    return {"tokens": t(tokens, torch.int32), "argmax": t(argmax, torch.int32),
+            "conf": t(conf.astype(np.float32), torch.float32),
+            "seed_idx": t(seed_idx, torch.int32), "n_seed": t(n_seed, torch.int32),
+            "remask_count": t(rng.integers(0, 4, (B, Lr)), torch.int32),
+            "mask_id": mask_id, "pos_offset": pos_offset}

@@ -170,3 +170,29 @@ def test_attn_stats_rejects_missing_buffers():
     assert _stats(good, ws=None) == cover.COVER_ERR_INVALID
     assert _stats(good, lse=None) == cover.COVER_ERR_INVALID
     assert cover.attn_stats_workspace(1, 32, 256) == 32 * 2 * 256
+
+
+def _upd(desc, tok=FAKE, si=FAKE, ns=FAKE, counts=None):
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return cover.lib().cover_decode_update(p(tok), p(FAKE), p(FAKE), p(si), p(ns), p(FAKE), None,
+                                           None, p(counts),
+                                           None if desc is None else ctypes.byref(desc), None)
+
+
+def test_decode_update_rejects_bad_arguments():
+    good = dict(B=1, Lr=256, max_seeds=16, pos_offset=768, mask_id=126463, draft_cap=15,
+                remask_budget=2, tau=0.9)
+    d = lambda **kw: cover.UpdateDesc(**{**good, **kw})
+    assert _upd(None) == cover.COVER_ERR_INVALID
+    assert _upd(d(B=-1)) == cover.COVER_ERR_INVALID
+    assert _upd(d(Lr=-1)) == cover.COVER_ERR_INVALID
+    assert _upd(d(max_seeds=-1)) == cover.COVER_ERR_INVALID
+    assert _upd(d(draft_cap=-1)) == cover.COVER_ERR_INVALID
+    assert _upd(d(tau=float("nan"))) == cover.COVER_ERR_INVALID
+    assert _upd(d(Lr=cover.COVER_MAX_LR + 1)) == cover.COVER_ERR_UNSUPPORTED
+    assert _upd(d(), tok=None) == cover.COVER_ERR_INVALID
+    assert _upd(d(), tok=FAKE + 2) == cover.COVER_ERR_INVALID
+    assert _upd(d(), si=None) == cover.COVER_ERR_INVALID
+    assert _upd(d(), ns=FAKE + 1) == cover.COVER_ERR_INVALID
+    assert _upd(d(), counts=FAKE + 2) == cover.COVER_ERR_INVALID
+    assert _upd(d(B=0), tok=None, si=None, ns=None) == cover.COVER_OK
