@@ -222,7 +222,7 @@ def attn_stats(q, k_live, k_cache, seed_idx, n_seed, r0, masked, drafted, scale=
 
 
 def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id, tau, cap,
-                  remask_budget, pos_offset=0):
+                  remask_budget, pos_offset=0, last_unmask=None):
     """One decoding step's state update over a region of Lr positions (absolute position =
     pos_offset + region index), for each batch row:
 
@@ -238,8 +238,14 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
     next selection's flags (Sec. 5.3, exclusion): bit 0 = unmasked after the update; bit 1 =
       i was a seed this step, or remask_count_i >= remask_budget.
 
+    flip-flops (Sec. 4, Definition): with last_unmask given (the token of each position's most
+      recent [MASK] -> token transition, -1 if none yet), a drafted position whose new token
+      equals its last_unmask entry is a flip-flop event; every drafted position then records
+      its new token there.  Replace is not an unmasking and leaves last_unmask alone.
+
     Confidences compare with tau in fp32.  Returns (tokens, remask_count, flags, drafted,
-    counts) with counts[b] = (|D|, kept, replaced, remasked, masked after the update).
+    counts) with counts[b] = (|D|, kept, replaced, remasked, masked after the update); with
+    last_unmask given, also (last_unmask, flipflops[b]).
     """
     tok = np.array(tokens, dtype=np.int64, copy=True)
     am = np.asarray(argmax, dtype=np.int64)
@@ -252,6 +258,8 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
     flags = np.zeros((B, Lr), np.uint8)
     drafted = np.zeros((B, Lr), np.uint8)
     counts = np.zeros((B, 5), np.int64)
+    last = None if last_unmask is None else np.array(last_unmask, dtype=np.int64, copy=True)
+    ff = np.zeros(B, np.int64)
     for b in range(B):
         # the previous step's seeds, as region indices (each counted once)
         seeds = set()
@@ -278,6 +286,10 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
         for i in D:
             tok[b, i] = am[b, i]
             drafted[b, i] = 1
+            if last is not None:
+                if last[b, i] == am[b, i]:
+                    ff[b] += 1
+                last[b, i] = am[b, i]
         for i in R:
             tok[b, i] = mask_id
             cnt[b, i] += 1
@@ -285,4 +297,7 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
             excl = i in seeds or cnt[b, i] >= remask_budget
             flags[b, i] = (1 if tok[b, i] != mask_id else 0) | (2 if excl else 0)
         counts[b] = (len(D), kept, replaced, len(R), int(np.sum(tok[b] == mask_id)))
-    return tok.astype(np.int32), cnt.astype(np.int32), flags, drafted, counts.astype(np.int32)
+    out = (tok.astype(np.int32), cnt.astype(np.int32), flags, drafted, counts.astype(np.int32))
+    if last is not None:
+        out = out + (last.astype(np.int32), ff.astype(np.int32))
+    return out

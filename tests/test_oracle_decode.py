@@ -17,14 +17,19 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "decode_examples.json
 def _run(e, fn=oracle.decode_update):
     a = lambda k, dt: np.array([e[k]], dtype=dt)
     si = np.array([e["seed_idx"]], np.int32).reshape(1, -1) if e["seed_idx"] else np.zeros((1, 0), np.int32)
+    kw = {"last_unmask": a("last_unmask", np.int32)} if "last_unmask" in e else {}
     return fn(a("tokens", np.int32), a("argmax", np.int32), a("conf", np.float32), si,
               np.array([e["n_seed"]], np.int32), a("remask_count", np.int32), e["mask_id"],
-              e["tau"], e["cap"], e["remask_budget"], e["pos_offset"])
+              e["tau"], e["cap"], e["remask_budget"], e["pos_offset"], **kw)
 
 
 def _golden_ok(fn):
     for e in json.load(open(GOLDEN))["examples"]:
-        tok, cnt, flags, drafted, counts = _run(e, fn)
+        r = _run(e, fn)
+        tok, cnt, flags, drafted, counts = r[:5]
+        if "last_unmask" in e and not (r[5][0].tolist() == e["out_last_unmask"]
+                                       and int(r[6][0]) == e["flipflops"]):
+            return False
         if not (tok[0].tolist() == e["out_tokens"] and cnt[0].tolist() == e["out_remask_count"]
                 and flags[0].tolist() == e["flags"] and drafted[0].tolist() == e["drafted"]
                 and counts[0].tolist() == e["counts"]):
@@ -110,6 +115,43 @@ def _mutant(old, new):
     return ns["decode_update"]
 
 
+def _history_ok(fn, seed, steps=40, Lr=48):
+    """Chained steps on one state with a small vocabulary (tokens recur): the flip-flops the
+    update reports add up to F counted from the definition over the recorded unmask history,
+    and every unmask event is a drafted position (sum of |D| = total unmask events)."""
+    rng = np.random.default_rng(seed)
+    mask_id = 5
+    tok = np.full((1, Lr), mask_id, np.int32)
+    cnt = np.zeros((1, Lr), np.int32)
+    last = np.full((1, Lr), -1, np.int32)
+    si, ns = np.full((1, 8), -1, np.int32), np.zeros(1, np.int32)
+    hist = [[] for _ in range(Lr)]
+    F = n_d = 0
+    for _ in range(steps):
+        am = rng.integers(0, mask_id, (1, Lr)).astype(np.int32)
+        conf = rng.choice(np.float32([0.5, 0.92, 0.97]), (1, Lr))
+        before = tok.copy()
+        tok, cnt, flags, drafted, counts, last, ff = fn(tok, am, conf, si, ns, cnt, mask_id, 0.9,
+                                                        6, 100, 0, last_unmask=last)
+        for i in range(Lr):
+            if before[0, i] == mask_id and tok[0, i] != mask_id:
+                hist[i].append(int(tok[0, i]))
+        F += int(ff[0])
+        n_d += int(counts[0, 0])
+        ok = np.nonzero(flags[0] & 1)[0]
+        k = min(8, ok.size)
+        si[0] = -1
+        si[0, :k] = rng.choice(ok, k, replace=False) if k else []
+        ns[0] = k
+    F_def = sum(sum(1 for a, b in zip(h, h[1:]) if a == b) for h in hist)
+    return F == F_def and n_d == sum(len(h) for h in hist) and F > 0
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_flip_flops_match_the_definition_over_a_history(seed):
+    assert _history_ok(oracle.decode_update, seed)
+
+
 MUTANTS = [
     ("draft_threshold_not_strict", "c[b, i] > t32]", "c[b, i] >= t32]"),
     ("draft_ties_larger_first", "(-float(c[b, i]), i)", "(-float(c[b, i]), -i)"),
@@ -120,6 +162,8 @@ MUTANTS = [
     ("budget_off_by_one", "cnt[b, i] >= remask_budget", "cnt[b, i] > remask_budget"),
     ("seed_not_excluded", "excl = i in seeds or", "excl ="),
     ("offset_ignored", "i = int(si[b, t]) - pos_offset", "i = int(si[b, t])"),
+    ("flip_flop_compares_wrong", "if last[b, i] == am[b, i]:", "if last[b, i] != am[b, i]:"),
+    ("flip_flop_not_recorded", "last[b, i] = am[b, i]", "pass"),
 ]
 
 
@@ -127,5 +171,6 @@ MUTANTS = [
 def test_pins_catch_planted_mistakes(name, old, new):
     fn = _mutant(old, new)
     caught = not _golden_ok(fn) or not all(_properties(fn, s, cap=cap) for s in range(5)
-                                           for cap in (5, 64))
+                                           for cap in (5, 64)) or \
+        not all(_history_ok(fn, s) for s in range(3))
     assert caught, name
