@@ -68,12 +68,15 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="llada", choices=["llada", "dream", "batched", "step"])
+    ap.add_argument("--workload", default="llada", choices=["llada", "dream", "batched", "step", "loop"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", choices=["attn", "select"], default=None)
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel", choices=["token_stats", "attn_stats"], default=None)
+    ap.add_argument("--lm-scale", type=float, default=8.0,
+                    help="loop workload: LM-head weights scaled by this (peaked distributions)")
+    ap.add_argument("--max-steps", type=int, default=512, help="loop workload: step budget")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -102,8 +105,8 @@ def main() -> int:
 
     if args.kernel:
         return bench_producer(args, dev, stream)
-    if args.workload == "step":
-        return bench_full_step(args, dev, stream)
+    if args.workload in ("step", "loop"):
+        return bench_full_step(args, dev, stream, loop=args.workload == "loop")
 
     a = synth.step_inputs(args.workload, seed=args.seed)
     c = a["cfg"]
@@ -309,7 +312,7 @@ def bench_producer(args, dev, stream) -> int:
     return 0
 
 
-def bench_full_step(args, dev, stream) -> int:
+def bench_full_step(args, dev, stream, loop: bool = False) -> int:
     """The full decode step of a random-init LLaDA-8B-shaped model (32 layers, hidden 4096, 32
     heads of 128, SwiGLU FFN 12288, RMSNorm, RoPE, vocabulary 126464; B=1, L=1024 = 768 prompt +
     256 generated, bf16): torch GEMMs and element-wise ops for the rest of the model, the COVER
@@ -369,7 +372,9 @@ def bench_full_step(args, dev, stream) -> int:
     as4 = lambda t: t.unsqueeze(0).permute(0, 2, 1, 3)  # [L, H, d] -> [1, H, L, d] view
     attn_ev = []
 
-    def step(parity: int, timed: bool):
+    def model(ids, parity: int, seed_idx, n_seed, timed: bool):
+        """The 32 layers on input ids; layer li's K/V go to kv[parity][li], its cache is
+        kv[1 - parity][li].  Returns the generated block's logits, the last layer's lse and q."""
         x = emb[ids]
         lse = q_last = None
         for li, ly in enumerate(layers):
@@ -394,7 +399,14 @@ def bench_full_step(args, dev, stream) -> int:
             gu = rmsnorm(x) @ ly["wgu"]
             x = x + (torch.nn.functional.silu(gu[:, :ffn]) * gu[:, ffn:]) @ ly["wd"]
             q_last = q
-        logits = rmsnorm(x[prompt:]) @ lm_head                       # [256, vocab]
+        return rmsnorm(x[prompt:]) @ lm_head, lse, q_last              # [256, vocab]
+
+    if loop:
+        return decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prompt, gen,
+                           mask_id, max_seeds, cap, n_layers)
+
+    def step(parity: int, timed: bool):
+        logits, lse, q_last = model(ids, parity, seed_idx, n_seed, timed)
         _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
         # drafting (at most 15 above 0.9), revision of the seeds, state update, flags
         tok_state, cnt_state = tok0.clone(), cnt0.clone()
@@ -440,6 +452,80 @@ def bench_full_step(args, dev, stream) -> int:
         "attn_flops_share": round(flops_attn / flops_step, 4),
         "step_tflops": round(flops_step / (step_ms * 1e-3) / 1e12, 1),
         "dtype": "bf16", "data": "synthetic (random-init weights N(0, 0.02), random token ids)"}))
+    return 0
+
+
+def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prompt, gen, mask_id,
+                max_seeds, cap, n_layers) -> int:
+    """COVER decoding of the 256-position block from all-[MASK] to completion on the random
+    model (Sec. 3 loop; Sec. 5.1-5.3 each step): the previous step's seeds enter as [MASK] and
+    read their K/V from the previous step's buffers, then token statistics, the state update
+    (drafting with cap 15 over tau 0.9, Keep/Replace/ReMask), the attention masses and the
+    next seeds.  The LM head is scaled by --lm-scale so that confidences spread over (0, 1]
+    (random weights otherwise give near-uniform distributions that never pass tau).  Reports
+    the step count T, the revision statistics and flip-flops F (Sec. 4), and checks the
+    Lemma A.1 bound T >= ceil((L + F) / B) and the unmask-count identity
+    sum_t |D_t| = L + #ReMask at completion."""
+    import numpy as np
+    import torch
+    from paper_2602_06161_amd import cover
+
+    tau, budget = 0.9, 2
+    prompt_ids = torch.from_numpy(tokens[:prompt]).to(dev)
+    tok = torch.full((1, gen), mask_id, dtype=torch.int32, device=dev)
+    cnt = torch.zeros((1, gen), dtype=torch.int32, device=dev)
+    last = torch.full((1, gen), -1, dtype=torch.int32, device=dev)
+    seed_idx = torch.full((1, max_seeds), -1, dtype=torch.int32, device=dev)
+    n_seed = torch.zeros(1, dtype=torch.int32, device=dev)
+    trash = torch.tensor([L], device=dev)
+    tot = np.zeros(6, np.int64)  # |D|, kept, replaced, remasked, (unused), flip-flops
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    T, done, idle = 0, False, 0
+    while T < args.max_steps and not done and idle < 32:
+        parity = T & 1
+        # model input: the prompt and the state, previous seeds fed as [MASK] (Sec. 5.1)
+        ids = torch.cat((prompt_ids, tok[0].long(), trash))
+        ids[torch.where(seed_idx[0] >= 0, seed_idx[0].long(), trash)] = mask_id
+        logits, lse, q_last = model(ids[:L], parity, seed_idx, n_seed, False)
+        logits = logits * args.lm_scale
+        _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
+        masked = (tok == mask_id).to(torch.uint8)
+        flags, drafted, counts, ff = cover.cover_decode_update(
+            tok, am[None], conf[None], seed_idx, n_seed, cnt, mask_id, tau, cap, budget, prompt,
+            last_unmask=last, stream=stream)
+        logp, _, _ = cover.cover_token_stats(logits, tok[0], want_conf=False, want_argmax=False,
+                                             stream=stream)
+        k_cur, _ = kv[parity][n_layers - 1]
+        k_prev, _ = kv[1 - parity][n_layers - 1]
+        d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx,
+                                             n_seed, lse, masked, drafted, prompt, stream=stream)
+        cover.cover_select_seeds(logp[None], d_in, d_out, flags, max_seeds, prompt,
+                                 seed_idx=seed_idx, n_seed=n_seed, want_score=False, stream=stream)
+        c = counts[0].cpu().numpy()
+        tot[:4] += c[:4]
+        tot[5] += int(ff[0].item())
+        T += 1
+        done = c[4] == 0
+        idle = idle + 1 if c[0] == 0 and c[3] == 0 else 0  # no draft and no ReMask: no progress
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    F = int(tot[5])
+    revisions = int(tot[2] + tot[3])
+    bound = -(-(gen + F) // cap)
+    print(json.dumps({
+        "workload": "COVER decoding loop, random-init LLaDA-8B-shaped model (32 layers), B=1, "
+                    f"prompt {prompt} + block {gen} from all [MASK], tau {tau}, cap {cap}, "
+                    f"ReMask budget {budget}, {max_seeds} seeds max, LM head x{args.lm_scale}",
+        "steps": T, "terminated": bool(done), "stalled": idle >= 32, "wall_s": round(wall, 3),
+        "ms_per_step": round(wall * 1e3 / T, 3), "tokens_per_s": round(gen / wall, 1),
+        "drafted": int(tot[0]), "kept": int(tot[1]), "replaced": int(tot[2]),
+        "remasked": int(tot[3]), "flip_flops": F, "total_revisions": revisions,
+        "effective_revisions": int(tot[2] + tot[3] - F),
+        "effective_revision_ratio": round((tot[2] + tot[3] - F) / revisions, 4) if revisions else None,
+        "lemma_a1_bound": bound, "lemma_a1_holds": bool(T >= bound) if done else None,
+        "unmask_identity_holds": bool(tot[0] == gen + tot[3]) if done else None,
+        "dtype": "bf16", "data": "synthetic (random-init weights, random prompt ids)"}))
     return 0
 
 

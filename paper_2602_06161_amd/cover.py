@@ -83,7 +83,8 @@ def lib():
         L.cover_select_seeds.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(SelectDesc), P]
         L.cover_select_seeds.restype = ctypes.c_int
         L.cover_token_stats.argtypes = [P, P, P, P, P, ctypes.POINTER(TokenDesc), P]
-        L.cover_decode_update.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.POINTER(UpdateDesc), P]
+        L.cover_decode_update.argtypes = [P, P, P, P, P, P, P, P, P, P, P,
+                                          ctypes.POINTER(UpdateDesc), P]
         L.cover_decode_update.restype = ctypes.c_int
         L.cover_token_stats.restype = ctypes.c_int
         L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
@@ -198,11 +199,13 @@ def cover_select_seeds(logp, d_in, d_out, flags, max_seeds: int, pos_offset: int
 def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id: int,
                         tau: float, draft_cap: int, remask_budget: int, pos_offset: int = 0,
                         flags=None, drafted=None, counts=None, want_outputs: bool = True,
-                        stream=None):
+                        last_unmask=None, flipflops=None, stream=None):
     """One step's decoding-state update, in place on tokens and remask_count (int32 [B,Lr]);
     argmax int32 / conf fp32 [B,Lr]; seed_idx int32 [B,max_seeds], n_seed int32 [B] (may be
     None: no seeds).  Returns (flags uint8, drafted uint8, counts int32 [B,5]), allocated
-    unless given (None when want_outputs is False)."""
+    unless given (None when want_outputs is False).  With last_unmask (int32 [B,Lr], in
+    place) the step's flip-flop events go to flipflops (int32 [B], allocated unless given),
+    returned as a fourth element."""
     B, Lr = tokens.shape
     for t, dt in ((tokens, torch.int32), (argmax, torch.int32), (conf, torch.float32),
                   (remask_count, torch.int32)):
@@ -221,17 +224,23 @@ def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, ma
         drafted = torch.empty((B, Lr), device=dev, dtype=torch.uint8) if drafted is None else drafted
         counts = torch.empty((B, 5), device=dev, dtype=torch.int32) if counts is None else counts
     for t, shape, dt in ((flags, (B, Lr), torch.uint8), (drafted, (B, Lr), torch.uint8),
-                         (counts, (B, 5), torch.int32)):
+                         (counts, (B, 5), torch.int32), (last_unmask, (B, Lr), torch.int32),
+                         (flipflops, (B,), torch.int32)):
         if t is not None and (t.shape != shape or t.dtype != dt or not t.is_contiguous()):
-            raise ValueError("flags/drafted must be contiguous uint8 [B,Lr], counts int32 [B,5]")
+            raise ValueError("flags/drafted must be contiguous uint8 [B,Lr], counts int32 [B,5], "
+                             "last_unmask int32 [B,Lr], flipflops int32 [B]")
+    if last_unmask is not None and flipflops is None:
+        flipflops = torch.empty((B,), device=dev, dtype=torch.int32)
     desc = UpdateDesc(B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget, tau)
     st = lib().cover_decode_update(_ptr(tokens), _ptr(argmax), _ptr(conf),
                                    _ptr(seed_idx) if max_seeds else None,
                                    _ptr(n_seed) if max_seeds else None, _ptr(remask_count),
-                                   _ptr(flags), _ptr(drafted), _ptr(counts), ctypes.byref(desc),
-                                   _stream(stream))
+                                   _ptr(flags), _ptr(drafted), _ptr(counts), _ptr(last_unmask),
+                                   _ptr(flipflops), ctypes.byref(desc), _stream(stream))
     if st != COVER_OK:
         raise CoverError(st, "cover_decode_update")
+    if last_unmask is not None:
+        return flags, drafted, counts, flipflops
     return flags, drafted, counts
 
 

@@ -186,8 +186,8 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
 cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const float* conf,
                                  const int32_t* seed_idx, const int32_t* n_seed,
                                  int32_t* remask_count, uint8_t* flags, uint8_t* drafted,
-                                 int32_t* counts, const cover_update_desc* desc,
-                                 hipStream_t stream) {
+                                 int32_t* counts, int32_t* last_unmask, int32_t* flipflops,
+                                 const cover_update_desc* desc, hipStream_t stream) {
   if (!desc) return COVER_ERR_INVALID;
   const cover_update_desc& D = *desc;
   if (D.B < 0 || D.Lr < 0 || D.max_seeds < 0 || D.draft_cap < 0) return COVER_ERR_INVALID;
@@ -202,11 +202,15 @@ cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const f
   if (D.max_seeds > 0 && (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4)))
     return COVER_ERR_INVALID;
   if (counts && !aligned(counts, 4)) return COVER_ERR_INVALID;
+  if (flipflops && ((!last_unmask && D.Lr > 0) || !aligned(flipflops, 4))) return COVER_ERR_INVALID;
+  if (last_unmask && D.Lr > 0 && !aligned(last_unmask, 4)) return COVER_ERR_INVALID;
   cover::UpdateArgs a;
   a.tokens = tokens; a.argmax = argmax; a.conf = conf;
   a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
   a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
   a.remask_count = remask_count; a.flags = flags; a.drafted = drafted; a.counts = counts;
+  a.last_unmask = D.Lr > 0 ? last_unmask : nullptr;
+  a.flipflops = flipflops;
   a.B = D.B; a.Lr = D.Lr; a.max_seeds = D.max_seeds; a.pos_offset = D.pos_offset;
   a.mask_id = D.mask_id; a.draft_cap = D.draft_cap; a.remask_budget = D.remask_budget;
   a.tau = D.tau;

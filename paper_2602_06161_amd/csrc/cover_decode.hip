@@ -4,8 +4,9 @@
 // One workgroup per batch row, every region position owned by one thread (positions
 // tid + m * nthreads, m < per), so all reads and writes are coalesced and the per-position
 // work needs no synchronisation.  The steps:
-//   1. the previous seeds become a bitmap of the region in LDS (entries outside the region or
-//      at masked positions are dropped, repeats collapse);
+//   1. the previous seeds become a bitmap of the region in LDS (entries outside the region are
+//      dropped, repeats collapse; a bit at a masked position is ignored in step 4), loaded
+//      while the tokens and confidences are in flight;
 //   2. the draft candidates (masked, confidence > tau in fp32) get a 64-bit key: the
 //      confidence mapped to an order-preserving unsigned integer in the high half, the
 //      bitwise complement of the position in the low half.  Keys are distinct and their
@@ -15,7 +16,9 @@
 //      256 bins), which stops at the first digit whose bucket is taken whole; the drafts are
 //      the keys at or above the prefix found;
 //   4. per position: drafting, revision of the seeds, ReMask counters, the next selection's
-//      flags, and the row's counts reduced through LDS.
+//      flags, flip-flop events (Sec. 4: a drafted token equal to the position's previous
+//      unmasked token) when the caller tracks that token, and the row's counts reduced
+//      through LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -38,6 +41,8 @@ struct UpdParams {
   uint8_t* flags;
   uint8_t* drafted;
   int32_t* counts;
+  int32_t* last_unmask;
+  int32_t* flipflops;
   int Lr, per, max_seeds, pos_offset, mask_id, cap, budget;
   float tau;
 };
@@ -58,43 +63,46 @@ __device__ __forceinline__ int wave_sum(int v) {
 __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdParams p) {
   __shared__ uint32_t seedbits[COVER_MAX_LR / 32];
   __shared__ uint32_t hist[256];
-  __shared__ int sums[6];  // candidates, |D|, kept, replaced, remasked, masked after
+  __shared__ int sums[7];  // candidates, |D|, kept, replaced, remasked, masked after, flip-flops
   __shared__ uint64_t s_prefix;
   __shared__ int s_need, s_done, s_shift;
 
   const int b = blockIdx.x, tid = threadIdx.x, nth = blockDim.x, lane = tid & 63;
   const int64_t base = (int64_t)b * p.Lr;
   for (int w = tid; w < (p.Lr + 31) / 32; w += nth) seedbits[w] = 0u;
-  if (tid < 6) sums[tid] = 0;
+  if (tid < 7) sums[tid] = 0;
   __syncthreads();
 
-  // 1. seed bitmap (reads the tokens before any thread writes them)
-  int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
-  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
-  for (int t = tid; t < ns; t += nth) {
-    const int64_t i = (int64_t)p.seed_idx[(int64_t)b * p.max_seeds + t] - p.pos_offset;
-    if (i >= 0 && i < p.Lr && p.tokens[base + i] != p.mask_id)
-      atomicOr(&seedbits[i >> 5], 1u << (i & 31));
-  }
-
-  // 2. candidate keys
+  // 1. per-position inputs, and the seed bitmap
   int tok[kMaxPer];
   float cf[kMaxPer];
-  uint64_t key[kMaxPer];
-  uint32_t cand = 0;
 #pragma unroll
   for (int m = 0; m < kMaxPer; ++m) {
     const int j = tid + m * nth;
     tok[m] = 0;
     cf[m] = 0.0f;
-    key[m] = 0;
     if (m < p.per && j < p.Lr) {
       tok[m] = p.tokens[base + j];
       cf[m] = p.conf[base + j];
-      if (tok[m] == p.mask_id && cf[m] > p.tau) {
-        cand |= 1u << m;
-        key[m] = ((uint64_t)ordered(cf[m]) << 32) | (uint32_t)~(uint32_t)j;
-      }
+    }
+  }
+  int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
+  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+  for (int t = tid; t < ns; t += nth) {
+    const int64_t i = (int64_t)p.seed_idx[(int64_t)b * p.max_seeds + t] - p.pos_offset;
+    if (i >= 0 && i < p.Lr) atomicOr(&seedbits[i >> 5], 1u << (i & 31));
+  }
+
+  // 2. candidate keys
+  uint64_t key[kMaxPer];
+  uint32_t cand = 0;
+#pragma unroll
+  for (int m = 0; m < kMaxPer; ++m) {
+    const int j = tid + m * nth;
+    key[m] = 0;
+    if (m < p.per && j < p.Lr && tok[m] == p.mask_id && cf[m] > p.tau) {
+      cand |= 1u << m;
+      key[m] = ((uint64_t)ordered(cf[m]) << 32) | (uint32_t)~(uint32_t)j;
     }
   }
   const int nc = wave_sum(__builtin_popcount(cand));
@@ -157,14 +165,15 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   }
 
   // 4. per-position update
-  int n_d = 0, n_keep = 0, n_rep = 0, n_rm = 0, n_masked = 0;
+  int n_d = 0, n_keep = 0, n_rep = 0, n_rm = 0, n_masked = 0, n_ff = 0;
 #pragma unroll
   for (int m = 0; m < kMaxPer; ++m) {
     const int j = tid + m * nth;
     if (m < p.per && j < p.Lr) {
       const int64_t e = base + j;
       const bool dr = !none && ((cand >> m) & 1u) && (key[m] & keep_mask) >= prefix;
-      const bool seed = (seedbits[j >> 5] >> (j & 31)) & 1u;
+      // a listed seed at a masked position is no seed
+      const bool seed = ((seedbits[j >> 5] >> (j & 31)) & 1u) && tok[m] != p.mask_id;
       int t = tok[m];
       int cnt = p.remask_count[e];
       if (dr || seed) {
@@ -172,6 +181,10 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
         if (dr) {
           t = a;
           ++n_d;
+          if (p.last_unmask) {
+            n_ff += p.last_unmask[e] == a ? 1 : 0;
+            p.last_unmask[e] = a;
+          }
         } else if (a == t) {
           ++n_keep;
         } else if (cf[m] > p.tau) {
@@ -191,15 +204,16 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
       if (p.drafted) p.drafted[e] = dr ? 1 : 0;
     }
   }
-  if (p.counts) {
-    const int v[5] = {n_d, n_keep, n_rep, n_rm, n_masked};
+  if (p.counts || p.flipflops) {
+    const int v[6] = {n_d, n_keep, n_rep, n_rm, n_masked, n_ff};
 #pragma unroll
-    for (int k = 0; k < 5; ++k) {
+    for (int k = 0; k < 6; ++k) {
       const int s = wave_sum(v[k]);
       if (lane == 0 && s) atomicAdd(&sums[1 + k], s);
     }
     __syncthreads();
-    if (tid < 5) p.counts[(int64_t)b * 5 + tid] = sums[1 + tid];
+    if (p.counts && tid < 5) p.counts[(int64_t)b * 5 + tid] = sums[1 + tid];
+    if (p.flipflops && tid == 0) p.flipflops[b] = sums[6];
   }
 }
 
@@ -210,6 +224,7 @@ hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream) {
   p.tokens = a.tokens; p.argmax = a.argmax; p.conf = a.conf;
   p.seed_idx = a.seed_idx; p.n_seed = a.n_seed; p.remask_count = a.remask_count;
   p.flags = a.flags; p.drafted = a.drafted; p.counts = a.counts;
+  p.last_unmask = a.last_unmask; p.flipflops = a.flipflops;
   p.Lr = a.Lr; p.max_seeds = a.max_seeds; p.pos_offset = a.pos_offset; p.mask_id = a.mask_id;
   p.cap = a.draft_cap; p.budget = a.remask_budget; p.tau = a.tau;
   int nth = ((a.Lr + 63) / 64) * 64;

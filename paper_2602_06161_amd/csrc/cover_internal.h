@@ -70,6 +70,8 @@ struct UpdateArgs {
   uint8_t* flags;    // may be null
   uint8_t* drafted;  // may be null
   int32_t* counts;   // may be null
+  int32_t* last_unmask;  // may be null
+  int32_t* flipflops;    // may be null (always null when last_unmask is)
   int32_t B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget;
   float tau;
 };
