@@ -271,15 +271,21 @@ typedef struct {
  *   [B,max_seeds] and n_seed int32 [B] (the seeds of the step, as cover_select_seeds
  *   emits them; may be NULL when max_seeds == 0), remask_count int32 (in/out),
  *   flags uint8 (out, may be NULL), drafted uint8 (out, 1 = drafted this step, may be NULL),
- *   counts int32 [B,5] (out, may be NULL): |D|, kept, replaced, remasked, masked after.
+ *   counts int32 [B,5] (out, may be NULL): |D|, kept, replaced, remasked, masked after;
+ *   last_unmask int32 (in/out, may be NULL): the token of each position's most recent
+ *   [MASK] -> token transition (-1 = none yet); every drafted position records its new
+ *   token (Replace is not an unmasking and leaves it alone);
+ *   flipflops int32 [B] (out, may be NULL; needs last_unmask): flip-flop events of the
+ *   step (Sec. 4 definition): drafted positions whose new token equals their last_unmask
+ *   entry on entry.
  * One kernel launch on `stream`; every result is an exact function of the inputs.  n_seed
  * values outside [0, max_seeds] are clamped.
  */
 cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const float* conf,
                                  const int32_t* seed_idx, const int32_t* n_seed,
                                  int32_t* remask_count, uint8_t* flags, uint8_t* drafted,
-                                 int32_t* counts, const cover_update_desc* desc,
-                                 hipStream_t stream);
+                                 int32_t* counts, int32_t* last_unmask, int32_t* flipflops,
+                                 const cover_update_desc* desc, hipStream_t stream);
 
 /*
  * cover_debug_status -- the contract checks enabled by COVER_DEBUG=1 (a debugging aid for

@@ -172,10 +172,10 @@ def test_attn_stats_rejects_missing_buffers():
     assert cover.attn_stats_workspace(1, 32, 256) == 32 * 2 * 256
 
 
-def _upd(desc, tok=FAKE, si=FAKE, ns=FAKE, counts=None):
+def _upd(desc, tok=FAKE, si=FAKE, ns=FAKE, counts=None, last=None, ff=None):
     p = lambda x: None if x is None else ctypes.c_void_p(x)
     return cover.lib().cover_decode_update(p(tok), p(FAKE), p(FAKE), p(si), p(ns), p(FAKE), None,
-                                           None, p(counts),
+                                           None, p(counts), p(last), p(ff),
                                            None if desc is None else ctypes.byref(desc), None)
 
 
@@ -195,4 +195,6 @@ def test_decode_update_rejects_bad_arguments():
     assert _upd(d(), si=None) == cover.COVER_ERR_INVALID
     assert _upd(d(), ns=FAKE + 1) == cover.COVER_ERR_INVALID
     assert _upd(d(), counts=FAKE + 2) == cover.COVER_ERR_INVALID
+    assert _upd(d(), ff=FAKE) == cover.COVER_ERR_INVALID              # flip-flops need last_unmask
+    assert _upd(d(), last=FAKE + 2, ff=FAKE) == cover.COVER_ERR_INVALID
     assert _upd(d(B=0), tok=None, si=None, ns=None) == cover.COVER_OK

@@ -14,22 +14,27 @@ from paper_2602_06161_amd import cover, synth
 pytestmark = pytest.mark.gpu
 
 
-def _both(a, tau, cap, budget, seeds=True):
+def _both(a, tau, cap, budget, seeds=True, last=None):
     announce(f"decode update B{a['tokens'].shape[0]} Lr{a['tokens'].shape[1]} tau{tau} cap{cap}")
     si = a["seed_idx"] if seeds else np.zeros((a["tokens"].shape[0], 0), np.int32)
     ns = a["n_seed"] if seeds else np.zeros(a["tokens"].shape[0], np.int32)
     exp = oracle.decode_update(a["tokens"].numpy(), a["argmax"].numpy(), a["conf"].numpy(),
                                np.asarray(si), np.asarray(ns), a["remask_count"].numpy(),
-                               a["mask_id"], tau, cap, budget, a["pos_offset"])
+                               a["mask_id"], tau, cap, budget, a["pos_offset"],
+                               **({} if last is None else {"last_unmask": last}))
     tok, cnt = a["tokens"].cuda(), a["remask_count"].cuda()
-    flags, drafted, counts = cover.cover_decode_update(
+    lt = None if last is None else torch.from_numpy(np.ascontiguousarray(last)).cuda()
+    r = cover.cover_decode_update(
         tok, a["argmax"].cuda(), a["conf"].cuda(), a["seed_idx"].cuda() if seeds else None,
         a["n_seed"].cuda() if seeds else None, cnt, a["mask_id"], tau, cap, budget,
-        a["pos_offset"])
+        a["pos_offset"], last_unmask=lt)
     torch.cuda.synchronize()
-    got = (tok.cpu().numpy(), cnt.cpu().numpy(), flags.cpu().numpy(), drafted.cpu().numpy(),
-           counts.cpu().numpy())
-    for name, g, e in zip(("tokens", "remask_count", "flags", "drafted", "counts"), got, exp):
+    got = (tok.cpu().numpy(), cnt.cpu().numpy(), r[0].cpu().numpy(), r[1].cpu().numpy(),
+           r[2].cpu().numpy())
+    if last is not None:
+        got = got + (lt.cpu().numpy(), r[3].cpu().numpy())
+    names = ("tokens", "remask_count", "flags", "drafted", "counts", "last_unmask", "flipflops")
+    for name, g, e in zip(names, got, exp):
         assert np.array_equal(g, e), f"{name}: {np.argwhere(g != e)[:8].tolist()}"
     return got
 
@@ -85,12 +90,16 @@ def test_negative_confidences_and_threshold():
 
 
 def test_chained_steps_keep_state():
-    # five steps on one state: each step's tokens, counters and flags feed the next
-    a = synth.update_inputs(2, 256, seed=21)
-    for t in range(5):
-        nxt = synth.update_inputs(2, 256, seed=100 + t)
+    # twelve steps on one state: each step's tokens, counters, flags and last unmasked tokens
+    # feed the next; a vocabulary of 4 makes restored tokens (flip-flops) common
+    a = synth.update_inputs(2, 256, seed=21, vocab=5)
+    last = np.full((2, 256), -1, np.int32)
+    total_ff = 0
+    for t in range(12):
+        nxt = synth.update_inputs(2, 256, seed=100 + t, vocab=5)
         a["argmax"], a["conf"] = nxt["argmax"], nxt["conf"]
-        tok, cnt, flags, drafted, _ = _both(a, 0.8, 12, 2)
+        tok, cnt, flags, drafted, _, last, ff = _both(a, 0.5, 40, 3, last=last)
+        total_ff += int(ff.sum())
         a["tokens"], a["remask_count"] = torch.from_numpy(tok), torch.from_numpy(cnt)
         # next seeds: unmasked, not excluded positions (any such set is a valid selection)
         for b in range(2):
@@ -98,3 +107,4 @@ def test_chained_steps_keep_state():
             a["seed_idx"][b] = -1
             a["seed_idx"][b, :ok.size] = torch.from_numpy(768 + ok.astype(np.int32))
             a["n_seed"][b] = ok.size
+    assert total_ff > 0
