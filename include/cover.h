@@ -233,6 +233,48 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
                               const cover_stats_desc* desc, hipStream_t stream);
 
 /*
+ * Block-query attention description: the attention problem of cover_attn_fwd (same fields
+ * and stride rules, with attn.L the number of keys; q and out hold Lq rows at the q strides)
+ * plus the query block [q_off, q_off + Lq) and the number of key splits.
+ *   q_off, Lq   0 <= q_off, 0 <= Lq, q_off + Lq <= attn.L (Lq == 0 is a no-op)
+ *   n_split     1 <= n_split <= 256: the keys are cut into n_split ranges processed in
+ *               parallel and merged (more splits fill the GPU when Lq is small)
+ */
+typedef struct {
+  cover_attn_desc attn;
+  int32_t q_off, Lq;
+  int32_t n_split;
+} cover_rect_desc;
+
+/* 4-byte words per (row, split) record of the cover_attn_rect workspace. */
+#define COVER_RECT_RECORD 68
+/* Workspace of cover_attn_rect in floats. */
+#define COVER_ATTN_RECT_WORKSPACE(B, Hq, Lq, n_split) \
+  ((int64_t)(B) * (Hq) * (n_split) * (Lq) * COVER_RECT_RECORD)
+
+/*
+ * cover_attn_rect -- COVER attention for one block of query rows against all L keys (the
+ * prefix-cache decoding COVER is combined with in Sec. 6.6: the block's rows are recomputed,
+ * the other positions' keys and values are reused).
+ *
+ * Row r of out/lse is row q_off + r of what cover_attn_fwd computes for a length-L sequence
+ * with the same k_live, v_live, k_cache, v_cache and seeds (Sec. 5.1 override memory and
+ * the leave-one-out diagonal of a seed row, App. B): q holds only the block's Lq rows.
+ * Seeds may lie anywhere in [0, L), inside the block or not.
+ * Arguments as for cover_attn_fwd; out [B,Hq,Lq,d] at the q strides; lse fp32 [B,Hq,Lq]
+ * contiguous (may be NULL); workspace: device fp32 buffer of
+ * COVER_ATTN_RECT_WORKSPACE(B, Hq, Lq, n_split) floats owned by the caller (contents on
+ * entry ignored, on exit unspecified).  Two kernel launches on `stream` (partial results
+ * per key split, then a merge in a fixed order: deterministic).
+ * Returns COVER_ERR_UNSUPPORTED for a dtype other than bf16, d != 128 or L > COVER_MAX_L.
+ */
+cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_live,
+                             const void* k_cache, const void* v_cache,
+                             const int32_t* seed_idx, const int32_t* n_seed,
+                             void* out, float* lse, float* workspace,
+                             const cover_rect_desc* desc, hipStream_t stream);
+
+/*
  * Decoding-state update description.
  *   B              batch rows (>= 0; 0 is a no-op)
  *   Lr             region length per row (>= 0, <= COVER_MAX_LR)

@@ -33,6 +33,7 @@ SOURCES = {
     "api.cpp": ["-x", "hip"],
     "cover_attn.hip": [],
     "cover_attn_w4.hip": [],
+    "cover_attn_rect.hip": [],
     "cover_debug.hip": [],
     "cover_decode.hip": [],
     "cover_select.hip": ["-ffp-contract=off"],  # the selection is bit-exact fp64

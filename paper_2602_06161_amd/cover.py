@@ -18,8 +18,9 @@ COVER_OK, COVER_ERR_INVALID, COVER_ERR_UNSUPPORTED, COVER_ERR_HIP = 0, -1, -2, -
 COVER_F32, COVER_BF16 = 0, 1
 COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
+COVER_RECT_RECORD = 68
 
-EXPORTED = ("cover_attn_fwd", "cover_attn_stats", "cover_debug_status", "cover_decode_update",
+EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_debug_status", "cover_decode_update",
             "cover_select_seeds", "cover_status_str", "cover_token_stats", "cover_version")
 # status bits of the contract checks that COVER_DEBUG=1 enables (cover_debug_status)
 COVER_DEBUG_SEED_COUNT, COVER_DEBUG_SEED_RANGE, COVER_DEBUG_SEED_DUPLICATE = 1, 2, 4
@@ -57,6 +58,11 @@ class UpdateDesc(ctypes.Structure):
                 ("tau", ctypes.c_float)]
 
 
+class RectDesc(ctypes.Structure):
+    _fields_ = [("attn", AttnDesc), ("q_off", ctypes.c_int32), ("Lq", ctypes.c_int32),
+                ("n_split", ctypes.c_int32)]
+
+
 class StatsDesc(ctypes.Structure):
     _fields_ = [("attn", AttnDesc), ("r0", ctypes.c_int32), ("Lr", ctypes.c_int32)]
 
@@ -83,6 +89,8 @@ def lib():
         L.cover_select_seeds.argtypes = [P, P, P, P, P, P, P, ctypes.POINTER(SelectDesc), P]
         L.cover_select_seeds.restype = ctypes.c_int
         L.cover_token_stats.argtypes = [P, P, P, P, P, ctypes.POINTER(TokenDesc), P]
+        L.cover_attn_rect.argtypes = [P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(RectDesc), P]
+        L.cover_attn_rect.restype = ctypes.c_int
         L.cover_decode_update.argtypes = [P, P, P, P, P, P, P, P, P, P, P,
                                           ctypes.POINTER(UpdateDesc), P]
         L.cover_decode_update.restype = ctypes.c_int
@@ -166,6 +174,61 @@ def cover_attn_fwd(q, k_live, v_live, k_cache, v_cache, seed_idx=None, n_seed=No
                               ctypes.byref(desc), _stream(stream))
     if st != COVER_OK:
         raise CoverError(st, "cover_attn_fwd")
+    return out, lse
+
+
+def rect_workspace(B: int, Hq: int, Lq: int, n_split: int) -> int:
+    """Floats of workspace cover_attn_rect needs (COVER_ATTN_RECT_WORKSPACE)."""
+    return B * Hq * n_split * Lq * COVER_RECT_RECORD
+
+
+def rect_splits(B: int, Hq: int, Lq: int, L: int) -> int:
+    """Key splits: about 256 workgroups in all, but splits of at least 128 keys, and no more
+    than about L / (2 Lq), so that the split records (Lq rows of 272 bytes per split, written
+    and read back) stay small against the K/V rows (512 bytes per key)."""
+    wgs = B * Hq * ((Lq + 127) // 128)
+    n = min(-(-256 // wgs), max(1, L // (2 * Lq)), -(-L // 128))
+    return max(1, min(n, 256))
+
+
+def cover_attn_rect(q, k_live, v_live, k_cache, v_cache, q_off: int, seed_idx=None, n_seed=None,
+                    out=None, lse=None, scale: float = 0.0, n_split=None, workspace=None,
+                    want_lse: bool = True, stream=None):
+    """COVER attention of the query block [q_off, q_off + Lq) against all L keys.  q
+    [B,Hq,Lq,d] bf16; k/v [B,Hkv,L,d] (equal strides); seeds as for cover_attn_fwd (absolute
+    positions).  Returns (out [B,Hq,Lq,d], lse [B,Hq,Lq])."""
+    for t in (k_live, v_live, k_cache, v_cache):
+        if t.shape != k_live.shape or t.stride() != k_live.stride() or t.dtype != q.dtype:
+            raise ValueError("k_live, v_live, k_cache, v_cache need equal shape, strides and dtype")
+    if q.stride(-1) != 1 or k_live.stride(-1) != 1:
+        raise ValueError("head dimension must be contiguous")
+    max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+    if seed_idx is not None and (seed_idx.dtype != torch.int32 or n_seed is None
+                                 or n_seed.dtype != torch.int32 or not seed_idx.is_contiguous()):
+        raise ValueError("seed_idx and n_seed must be contiguous int32 tensors")
+    B, Hq, Lq, d = q.shape
+    L = k_live.shape[2]
+    if out is None:
+        out = torch.empty_like(q)
+    if out.shape != q.shape or out.stride() != q.stride() or out.dtype != q.dtype:
+        raise ValueError("out must match q's shape, strides and dtype")
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, Lq), device=q.device, dtype=torch.float32)
+    if n_split is None:
+        n_split = rect_splits(B, Hq, Lq, L)
+    need = rect_workspace(B, Hq, Lq, n_split)
+    if workspace is None:
+        workspace = torch.empty(max(need, 4), device=q.device, dtype=torch.float32)
+    if workspace.dtype != torch.float32 or workspace.numel() < need or not workspace.is_contiguous():
+        raise ValueError(f"workspace must be contiguous fp32 with at least {need} elements")
+    ad = attn_desc(q, k_live, max_seeds, scale)
+    ad.L = L
+    desc = RectDesc(ad, q_off, Lq, n_split)
+    st = lib().cover_attn_rect(_ptr(q), _ptr(k_live), _ptr(v_live), _ptr(k_cache), _ptr(v_cache),
+                               _ptr(seed_idx), _ptr(n_seed), _ptr(out), _ptr(lse), _ptr(workspace),
+                               ctypes.byref(desc), _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_attn_rect")
     return out, lse
 
 

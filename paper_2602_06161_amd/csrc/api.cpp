@@ -183,6 +183,53 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
   return hip_status(cover::launch_attn_stats(a, stream));
 }
 
+cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_live,
+                             const void* k_cache, const void* v_cache,
+                             const int32_t* seed_idx, const int32_t* n_seed,
+                             void* out, float* lse, float* workspace,
+                             const cover_rect_desc* desc, hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_attn_desc& D = desc->attn;
+  const int32_t q_off = desc->q_off, Lq = desc->Lq, n_split = desc->n_split;
+  if (D.B < 0 || D.L < 0 || D.Hq < 1 || D.Hkv < 1 || D.d < 1 || D.max_seeds < 0)
+    return COVER_ERR_INVALID;
+  if (D.Hq % D.Hkv != 0) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_F32 && D.dtype != COVER_BF16) return COVER_ERR_INVALID;
+  if (!(D.scale >= 0.0f) || isinf(D.scale)) return COVER_ERR_INVALID;
+  if (q_off < 0 || Lq < 0 || (int64_t)q_off + Lq > D.L) return COVER_ERR_INVALID;
+  if (n_split < 1 || n_split > 256) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_BF16 || D.d != 128) return COVER_ERR_UNSUPPORTED;
+  if (D.L > COVER_MAX_L) return COVER_ERR_UNSUPPORTED;
+  if (D.B == 0 || Lq == 0) return COVER_OK;
+  const void* tensors[6] = {q, k_live, v_live, k_cache, v_cache, out};
+  for (const void* t : tensors)
+    if (!t || !aligned(t, 16)) return COVER_ERR_INVALID;
+  const int64_t strides[6] = {D.q_sb, D.q_sh, D.q_sl, D.kv_sb, D.kv_sh, D.kv_sl};
+  for (int64_t s : strides)
+    if (s < 0 || s % 8 != 0) return COVER_ERR_INVALID;
+  if ((Lq > 1 && D.q_sl < D.d) || (D.L > 1 && D.kv_sl < D.d)) return COVER_ERR_INVALID;
+  if (D.max_seeds > 0 && (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4)))
+    return COVER_ERR_INVALID;
+  if (lse && !aligned(lse, 4)) return COVER_ERR_INVALID;
+  if (!workspace || !aligned(workspace, 16)) return COVER_ERR_INVALID;
+  if ((int64_t)D.B * D.Hq * ((Lq + 127) / 128) * n_split > 0x7fffffffLL) return COVER_ERR_UNSUPPORTED;
+  cover::RectArgs a;
+  a.q = q; a.k_live = k_live; a.v_live = v_live; a.k_cache = k_cache; a.v_cache = v_cache;
+  a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
+  a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
+  a.out = out; a.lse = lse; a.workspace = workspace;
+  a.B = D.B; a.Hq = D.Hq; a.Hkv = D.Hkv; a.L = D.L; a.max_seeds = D.max_seeds;
+  a.q_off = q_off; a.Lq = Lq; a.n_split = n_split;
+  a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
+  a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
+  a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  if (cover::debug_enabled()) {
+    const hipError_t e = cover::launch_check_seeds(a.seed_idx, a.n_seed, D.B, D.max_seeds, D.L, stream);
+    if (e != hipSuccess) return COVER_ERR_HIP;
+  }
+  return hip_status(cover::launch_attn_rect(a, stream));
+}
+
 cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const float* conf,
                                  const int32_t* seed_idx, const int32_t* n_seed,
                                  int32_t* remask_count, uint8_t* flags, uint8_t* drafted,

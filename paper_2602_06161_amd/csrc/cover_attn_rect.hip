@@ -1,0 +1,335 @@
+// COVER attention for a block of queries against the whole sequence (the prefix-cache
+// decoding combined with COVER in Sec. 6.6: only the current block's rows are recomputed; the
+// prompt's keys and values come from the caller's cache), bf16, head size 128, on gfx950.
+//
+// Per query row i at absolute position p = q_off + r the result is the row p of the square
+// COVER attention (Sec. 5.1): keys and values of seed positions come from the cache, every
+// other position's from the live tensors, and a seed row sees its own live key and value on
+// its diagonal (the leave-one-out view whose closed form App. B.4 gives).
+//
+// With few query rows the work is bound by reading K and V once, not by the MFMAs, and one
+// workgroup per (row, query tile) would leave most of the chip idle, so the keys are split:
+//   * kernel 1: one workgroup of 4 waves per (batch, query head, 128-query tile, key split).
+//     The waves share the split's K/V in LDS, loaded in groups of up to four 32-key stages
+//     (128 keys, 64 KiB) that are all requested at once, so a group costs one memory round
+//     trip; wave w owns 32 queries.  The Q rows and the seed list are requested together at
+//     the start.  S^T = K Q^T and O^T += V^T P^T
+//     on 32x32x16 bf16 MFMAs (Q as the B operand straight from registers, V^T by transposing
+//     LDS reads, P^T from the S^T registers), online softmax with the row max, row sums and
+//     O^T in fp32.  A seed row's cached diagonal score is dropped where it occurs and its
+//     live diagonal term is added by the split that holds the position.  Per row the split
+//     leaves its normalised output O / l in bf16 (256 bytes) and its max and sum in fp32 in
+//     the caller's workspace: the records are written and read once, so their size is
+//     traffic on top of K and V.
+//   * kernel 2: one wave per query row merges the splits and writes O and the lse.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace cover {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_t;
+
+constexpr int kD = 128;
+constexpr int kRow = 2 * kD;            // bytes per K/V row
+constexpr int kStage = 32;              // keys per stage
+constexpr int kGroup = 4;               // stages loaded together
+constexpr int kThreads = 256;           // 4 waves
+constexpr int kQT = 128;                // queries per workgroup
+constexpr int kMaxWords = COVER_MAX_L / 32;
+constexpr float kInit = -1.0e30f;       // finite "nothing seen yet" max
+constexpr float kLn2 = 0.693147180559945309f;
+
+struct RectParams {
+  const __bf16* q;
+  const __bf16* kl;
+  const __bf16* vl;
+  const __bf16* kc;
+  const __bf16* vc;
+  const int32_t* seed_idx;
+  const int32_t* n_seed;
+  float* ws;
+  __bf16* out;
+  float* lse;
+  int B, Hq, Hkv, L, Lq, q_off, max_seeds, group, n_qt, n_split, split_stages;
+  float c2;  // scale * log2(e)
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
+// LDS layouts: K rows with the 16-byte chunk index XOR-ed by row % 16 (a b128 operand read of
+// 32 rows covers all banks); V rows with the chunk index XOR-ed by 4 (row % 4) (a transposing
+// read of 8 rows x 64 bytes covers every bank twice).
+__device__ __forceinline__ uint32_t k_off(int row, int c) { return row * kRow + ((c ^ (row & 15)) << 4); }
+__device__ __forceinline__ uint32_t v_chunk(int row, int c) { return row * kRow + ((c ^ ((row & 3) << 2)) << 4); }
+__device__ __forceinline__ uint32_t v_elem(int row, int col) { return v_chunk(row, col >> 3) + ((col & 7) << 1); }
+
+__device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void cover_attn_rect_kernel(const RectParams p) {
+  __shared__ __attribute__((aligned(16))) char sK[kGroup][kStage * kRow];
+  __shared__ __attribute__((aligned(16))) char sV[kGroup][kStage * kRow];
+  __shared__ uint32_t bm[kMaxWords];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hl = lane >> 5;
+  int id = blockIdx.x;
+  const int qt = id % p.n_qt;
+  id /= p.n_qt;
+  const int split = id % p.n_split;
+  const int bh = id / p.n_split;
+  const int b = bh / p.Hq, h = bh % p.Hq, hk = h / p.group;
+
+  // this wave's queries (requested first: nothing below depends on them until the MFMAs)
+  const int qrow0 = qt * kQT + wave * 32;
+  const bool active = qrow0 < p.Lq;
+  const int qrow = min(qrow0 + l32, p.Lq - 1);
+  const int pos = p.q_off + qrow;
+  const __bf16* qp = p.q + b * p.q_sb + h * p.q_sh + (int64_t)qrow * p.q_sl;
+  bf16x8 qreg[kD / 16];
+#pragma unroll
+  for (int ks = 0; ks < kD / 16; ++ks)
+    qreg[ks] = *(const bf16x8*)(qp + (2 * ks + hl) * 8);
+
+  // seed bitmap of the whole sequence; the count and the list are requested together
+  const int nW = (p.L + 31) >> 5;
+  for (int w = tid; w < nW; w += kThreads) bm[w] = 0u;
+  __syncthreads();
+  if (p.max_seeds > 0) {
+    int ns = p.n_seed[b];
+    ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+    for (int t = tid; t < p.max_seeds; t += kThreads) {
+      const int j = p.seed_idx[(int64_t)b * p.max_seeds + t];
+      if (t < ns && j >= 0 && j < p.L) atomicOr(&bm[j >> 5], 1u << (j & 31));
+    }
+  }
+  __syncthreads();
+  auto is_seed = [&](int j) { return (bm[j >> 5] >> (j & 31)) & 1u; };
+  const bool row_seed = is_seed(pos);
+
+  // key range of this split
+  const int k_begin = split * p.split_stages * kStage;
+  const int k_end = min(p.L, k_begin + p.split_stages * kStage);
+  const int n_st = k_end > k_begin ? (k_end - k_begin + kStage - 1) / kStage : 0;
+
+  // cooperative group loads: per stage 512 chunks of 16 bytes of K (and of V), two per
+  // thread; every stage of a group is requested before the first is stored
+  const int64_t kvbase = b * p.kv_sb + hk * p.kv_sh;
+  auto load_group = [&](int st0, int n) {
+    u32x4 kr[kGroup][2], vr[kGroup][2];
+#pragma unroll
+    for (int g = 0; g < kGroup; ++g)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int c = tid * 2 + u, row = c >> 4, ch = c & 15;
+        const int key = k_begin + (st0 + g) * kStage + row;
+        kr[g][u] = vr[g][u] = u32x4{0u, 0u, 0u, 0u};
+        if (g < n && key < k_end) {
+          const int64_t off = kvbase + (int64_t)key * p.kv_sl + ch * 8;
+          const bool sd = is_seed(key);
+          kr[g][u] = *(const u32x4*)((sd ? p.kc : p.kl) + off);
+          vr[g][u] = *(const u32x4*)((sd ? p.vc : p.vl) + off);
+        }
+      }
+#pragma unroll
+    for (int g = 0; g < kGroup; ++g)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int c = tid * 2 + u, row = c >> 4, ch = c & 15;
+        if (g < n) {
+          *(u32x4*)(sK[g] + k_off(row, ch)) = kr[g][u];
+          *(u32x4*)(sV[g] + v_chunk(row, ch)) = vr[g][u];
+        }
+      }
+  };
+
+  // V^T operand addresses: lane (G = lane / 16, i = lane % 16) reads keys
+  // 16 kk + {0..3, 8..11} + 4 (G / 2) of d-block db, the key order of the S^T registers
+  uint32_t vaddr[kD / 32];
+  {
+    const int G = lane >> 4, ii = lane & 15;
+    const int row = 4 * (G >> 1) + (ii >> 2);
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) vaddr[db] = v_elem(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
+  }
+
+  f32x16 o[kD / 32];
+#pragma unroll
+  for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+  float m = kInit, l = 0.0f;
+
+  for (int st = 0; st < n_st; ++st) {
+    const int buf = st % kGroup;
+    if (buf == 0) {
+      if (st > 0) __syncthreads();  // every wave is done with the previous group
+      load_group(st, min(kGroup, n_st - st));
+      __syncthreads();
+    }
+    if (active) {
+      const lds_t* kb = (const lds_t*)sK[buf];
+      const lds_t* vb = (const lds_t*)sV[buf];
+      f32x16 s;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < kD / 16; ++ks) {
+        const bf16x8 a = *(const __attribute__((address_space(3))) bf16x8*)(kb + k_off(l32, 2 * ks + hl));
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s, 0, 0, 0);
+      }
+      // register r holds key k0 + 8 (r / 4) + 4 hl + r % 4 of query row qrow
+      const int k0 = k_begin + st * kStage;
+      float mx = kInit;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        float t = s[r] * p.c2;
+        if (key >= k_end || (row_seed && key == pos)) t = -INFINITY;
+        s[r] = t;
+        mx = __builtin_fmaxf(mx, t);
+      }
+      mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = __builtin_fmaxf(m, mx);
+      if (__builtin_amdgcn_ballot_w64(mn > m)) {  // some row's max grew: rescale
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      }
+      m = mn;
+      float pr[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        pr[r] = __builtin_amdgcn_exp2f(s[r] - m);
+        l += pr[r];
+      }
+      bf16x8 pk[2];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pk[kk][e] = (__bf16)pr[8 * kk + e];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int db = 0; db < kD / 32; ++db) {
+          const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
+          const bf16x8 va = __builtin_bit_cast(
+              bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pk[kk], o[db], 0, 0, 0);
+        }
+    }
+  }
+
+  if (!active) return;
+  // the live diagonal term of a seed row, in the split that holds its position
+  if (row_seed && pos >= k_begin && pos < k_end) {
+    const __bf16* kp = p.kl + kvbase + (int64_t)pos * p.kv_sl;
+    float dot = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < kD / 16; ++ks) {
+      const bf16x8 kv8 = *(const bf16x8*)(kp + (2 * ks + hl) * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dot = __builtin_fmaf((float)qreg[ks][e], (float)kv8[e], dot);
+    }
+    dot += __shfl_xor(dot, 32);
+    const float t = dot * p.c2;
+    const float mn = __builtin_fmaxf(m, t);
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);
+    m = mn;
+    const float pd = __builtin_amdgcn_exp2f(t - m);
+    l = l * alpha + (hl == 0 ? pd : 0.0f);
+    const __bf16* vp = p.vl + kvbase + (int64_t)pos * p.kv_sl;
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dim = 32 * db + 8 * g + 4 * hl;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[db][4 * g + e] = __builtin_fmaf(pd, (float)vp[dim + e], o[db][4 * g + e] * alpha);
+      }
+  }
+  const float lt = l + __shfl_xor(l, 32);
+  if (qrow0 + l32 >= p.Lq) return;
+  float* rec = p.ws + (((int64_t)bh * p.n_split + split) * p.Lq + qrow0 + l32) * COVER_RECT_RECORD;
+  const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+#pragma unroll
+  for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *(bf16x4*)((__bf16*)rec + 32 * db + 8 * g + 4 * hl) =
+          bf16x4{(__bf16)(o[db][4 * g] * inv), (__bf16)(o[db][4 * g + 1] * inv),
+                 (__bf16)(o[db][4 * g + 2] * inv), (__bf16)(o[db][4 * g + 3] * inv)};
+  if (hl == 0) {
+    rec[kD / 2] = m;
+    rec[kD / 2 + 1] = lt;
+  }
+}
+
+// One wave per query row: merge the splits' (max, sum, O / sum), write O (bf16) and the lse.
+__global__ __launch_bounds__(256) void cover_attn_rect_merge_kernel(const RectParams p) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // over B * Hq * Lq
+  if (row >= (int64_t)p.B * p.Hq * p.Lq) return;
+  const int64_t bh = row / p.Lq;
+  const int r = (int)(row % p.Lq);
+  const int b = (int)(bh / p.Hq), h = (int)(bh % p.Hq);
+  const float* rec0 = p.ws + (bh * p.n_split * p.Lq + r) * COVER_RECT_RECORD;
+  const int64_t sstride = (int64_t)p.Lq * COVER_RECT_RECORD;
+  float M = kInit;
+  for (int s = 0; s < p.n_split; ++s) M = __builtin_fmaxf(M, rec0[s * sstride + kD / 2]);
+  float den = 0.0f, o0 = 0.0f, o1 = 0.0f;
+  for (int s = 0; s < p.n_split; ++s) {
+    const float* rec = rec0 + s * sstride;
+    const float w = rec[kD / 2 + 1] * __builtin_amdgcn_exp2f(rec[kD / 2] - M);
+    const uint32_t pair = ((const uint32_t*)rec)[lane];  // bf16 O of dims 2 lane, 2 lane + 1
+    den += w;
+    o0 = __builtin_fmaf(__uint_as_float(pair << 16), w, o0);
+    o1 = __builtin_fmaf(__uint_as_float(pair & 0xffff0000u), w, o1);
+  }
+  const float inv = 1.0f / den;
+  __bf16* op = p.out + b * p.q_sb + h * p.q_sh + (int64_t)r * p.q_sl + 2 * lane;
+  op[0] = (__bf16)(o0 * inv);
+  op[1] = (__bf16)(o1 * inv);
+  if (p.lse && lane == 0) p.lse[row] = (M + __builtin_amdgcn_logf(den)) * kLn2;
+}
+
+}  // namespace
+
+hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream) {
+  RectParams p;
+  p.q = (const __bf16*)a.q; p.kl = (const __bf16*)a.k_live; p.vl = (const __bf16*)a.v_live;
+  p.kc = (const __bf16*)a.k_cache; p.vc = (const __bf16*)a.v_cache;
+  p.seed_idx = a.seed_idx; p.n_seed = a.n_seed; p.ws = a.workspace;
+  p.out = (__bf16*)a.out; p.lse = a.lse;
+  p.B = a.B; p.Hq = a.Hq; p.Hkv = a.Hkv; p.L = a.L; p.Lq = a.Lq; p.q_off = a.q_off;
+  p.max_seeds = a.max_seeds; p.group = a.Hq / a.Hkv;
+  p.n_qt = (a.Lq + kQT - 1) / kQT;
+  p.n_split = a.n_split;
+  const int stages = (a.L + kStage - 1) / kStage;
+  p.split_stages = (stages + a.n_split - 1) / a.n_split;
+  p.c2 = a.scale * 1.44269504088896341f;
+  p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
+  p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
+  const int64_t nwg = (int64_t)a.B * a.Hq * p.n_qt * a.n_split;
+  hipLaunchKernelGGL(cover_attn_rect_kernel, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t rows = (int64_t)a.B * a.Hq * a.Lq;
+  hipLaunchKernelGGL(cover_attn_rect_merge_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

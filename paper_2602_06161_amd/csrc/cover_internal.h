@@ -60,6 +60,22 @@ struct StatsArgs {
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
 
+struct RectArgs {
+  const void* q;
+  const void* k_live;
+  const void* v_live;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* seed_idx;  // may be null when max_seeds == 0
+  const int32_t* n_seed;    // may be null when max_seeds == 0
+  void* out;
+  float* lse;  // may be null
+  float* workspace;
+  int32_t B, Hq, Hkv, L, max_seeds, q_off, Lq, n_split;
+  float scale;  // > 0
+  int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
+};
+
 struct UpdateArgs {
   int32_t* tokens;
   const int32_t* argmax;
@@ -83,6 +99,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
 hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream);
+hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream);  // bf16, d = 128
 
 // contract checks (COVER_DEBUG=1)
 bool debug_enabled();

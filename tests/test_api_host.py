@@ -198,3 +198,31 @@ def test_decode_update_rejects_bad_arguments():
     assert _upd(d(), ff=FAKE) == cover.COVER_ERR_INVALID              # flip-flops need last_unmask
     assert _upd(d(), last=FAKE + 2, ff=FAKE) == cover.COVER_ERR_INVALID
     assert _upd(d(B=0), tok=None, si=None, ns=None) == cover.COVER_OK
+
+
+def _rect(desc, ws=FAKE):
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return cover.lib().cover_attn_rect(p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(FAKE),
+                                       p(FAKE), p(FAKE), None, p(ws),
+                                       None if desc is None else ctypes.byref(desc), None)
+
+
+@pytest.mark.parametrize("kw,q_off,Lq,n_split,expect", [
+    (dict(), -1, 8, 1, cover.COVER_ERR_INVALID),
+    (dict(), 60, 8, 1, cover.COVER_ERR_INVALID),            # q_off + Lq > L
+    (dict(), 0, -1, 1, cover.COVER_ERR_INVALID),
+    (dict(), 0, 8, 0, cover.COVER_ERR_INVALID),             # n_split < 1
+    (dict(), 0, 8, 257, cover.COVER_ERR_INVALID),
+    (dict(d=64), 0, 8, 1, cover.COVER_ERR_UNSUPPORTED),
+    (dict(dtype=cover.COVER_F32, q_sl=128, kv_sl=128), 0, 8, 1, cover.COVER_ERR_UNSUPPORTED),
+    (dict(), 0, 0, 1, cover.COVER_OK),                      # empty block: no-op
+])
+def test_attn_rect_rejects_bad_descriptors(kw, q_off, Lq, n_split, expect):
+    assert _rect(cover.RectDesc(_good(**kw), q_off, Lq, n_split)) == expect
+
+
+def test_attn_rect_needs_a_workspace():
+    assert _rect(None) == cover.COVER_ERR_INVALID
+    assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=None) == cover.COVER_ERR_INVALID
+    assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=FAKE + 4) == cover.COVER_ERR_INVALID
+    assert cover.rect_workspace(1, 32, 256, 4) == 32 * 4 * 256 * cover.COVER_RECT_RECORD
