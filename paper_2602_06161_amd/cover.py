@@ -183,11 +183,10 @@ def rect_workspace(B: int, Hq: int, Lq: int, n_split: int) -> int:
 
 
 def rect_splits(B: int, Hq: int, Lq: int, L: int) -> int:
-    """Key splits: about 256 workgroups in all, but splits of at least 128 keys, and no more
-    than about L / (2 Lq), so that the split records (Lq rows of 272 bytes per split, written
-    and read back) stay small against the K/V rows (512 bytes per key)."""
+    """Key splits: about 256 workgroups in all (one per compute unit; the split kernel is
+    bound by each workgroup's serial work, not by HBM), with at least 128 keys per split."""
     wgs = B * Hq * ((Lq + 127) // 128)
-    n = min(-(-256 // wgs), max(1, L // (2 * Lq)), -(-L // 128))
+    n = min(-(-256 // wgs), -(-L // 128))
     return max(1, min(n, 256))
 
 
