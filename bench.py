@@ -77,6 +77,9 @@ def main() -> int:
     ap.add_argument("--lm-scale", type=float, default=8.0,
                     help="loop workload: LM-head weights scaled by this (peaked distributions)")
     ap.add_argument("--max-steps", type=int, default=512, help="loop workload: step budget")
+    ap.add_argument("--variant", choices=["cover", "wo_kv", "wo_seed"], default="cover",
+                    help="loop workload: COVER, or the ablations of Sec. 6.4 (no KV override; "
+                         "confidence-drop seeds)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -514,7 +517,12 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     (random weights otherwise give near-uniform distributions that never pass tau).  Reports
     the step count T, the revision statistics and flip-flops F (Sec. 4), and checks the
     Lemma A.1 bound T >= ceil((L + F) / B) and the unmask-count identity
-    sum_t |D_t| = L + #ReMask at completion."""
+    sum_t |D_t| = L + #ReMask at completion.
+
+    --variant wo_kv: verification by masking the seeds in the input only (no KV override and
+    no diagonal rule: the attention is called without seeds).  --variant wo_seed: the seeds
+    are ranked by their confidence drop, log p at drafting minus log p now (same selection
+    kernel and budget rule, with zero attention masses)."""
     import numpy as np
     import torch
     from paper_2602_06161_amd import cover
@@ -527,6 +535,9 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     seed_idx = torch.full((1, max_seeds), -1, dtype=torch.int32, device=dev)
     n_seed = torch.zeros(1, dtype=torch.int32, device=dev)
     trash = torch.tensor([L], device=dev)
+    no_seeds = torch.zeros(1, dtype=torch.int32, device=dev)
+    logp_draft = torch.zeros((1, gen), dtype=torch.float32, device=dev)
+    zeros = torch.zeros((1, gen), dtype=torch.float32, device=dev)
     tot = np.zeros(6, np.int64)  # |D|, kept, replaced, remasked, (unused), flip-flops
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -536,7 +547,8 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         # model input: the prompt and the state, previous seeds fed as [MASK] (Sec. 5.1)
         ids = torch.cat((prompt_ids, tok[0].long(), trash))
         ids[torch.where(seed_idx[0] >= 0, seed_idx[0].long(), trash)] = mask_id
-        logits, lse, q_last = model(ids[:L], parity, seed_idx, n_seed, False)
+        attn_n = no_seeds if args.variant == "wo_kv" else n_seed
+        logits, lse, q_last = model(ids[:L], parity, seed_idx, attn_n, False)
         logits = logits * args.lm_scale
         _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
         masked = (tok == mask_id).to(torch.uint8)
@@ -545,12 +557,21 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
             last_unmask=last, stream=stream)
         logp, _, _ = cover.cover_token_stats(logits, tok[0], want_conf=False, want_argmax=False,
                                              stream=stream)
-        k_cur, _ = kv[parity][n_layers - 1]
-        k_prev, _ = kv[1 - parity][n_layers - 1]
-        d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx,
-                                             n_seed, lse, masked, drafted, prompt, stream=stream)
-        cover.cover_select_seeds(logp[None], d_in, d_out, flags, max_seeds, prompt,
-                                 seed_idx=seed_idx, n_seed=n_seed, want_score=False, stream=stream)
+        if args.variant == "wo_seed":
+            # confidence drop since drafting: log p at the unmasking minus log p now
+            logp_draft = torch.where(drafted == 1, logp[None], logp_draft)
+            cover.cover_select_seeds(logp[None] - logp_draft, zeros, zeros, flags, max_seeds,
+                                     prompt, seed_idx=seed_idx, n_seed=n_seed, want_score=False,
+                                     stream=stream)
+        else:
+            k_cur, _ = kv[parity][n_layers - 1]
+            k_prev, _ = kv[1 - parity][n_layers - 1]
+            d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx,
+                                                 attn_n, lse, masked, drafted, prompt,
+                                                 stream=stream)
+            cover.cover_select_seeds(logp[None], d_in, d_out, flags, max_seeds, prompt,
+                                     seed_idx=seed_idx, n_seed=n_seed, want_score=False,
+                                     stream=stream)
         c = counts[0].cpu().numpy()
         tot[:4] += c[:4]
         tot[5] += int(ff[0].item())
@@ -563,8 +584,8 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     revisions = int(tot[2] + tot[3])
     bound = -(-(gen + F) // cap)
     print(json.dumps({
-        "workload": "COVER decoding loop, random-init LLaDA-8B-shaped model (32 layers), B=1, "
-                    f"prompt {prompt} + block {gen} from all [MASK], tau {tau}, cap {cap}, "
+        "workload": f"{args.variant} decoding loop, random-init LLaDA-8B-shaped model (32 "
+                    f"layers), B=1, prompt {prompt} + block {gen} from all [MASK], tau {tau}, cap {cap}, "
                     f"ReMask budget {budget}, {max_seeds} seeds max, LM head x{args.lm_scale}",
         "steps": T, "terminated": bool(done), "stalled": idle >= 32, "wall_s": round(wall, 3),
         "ms_per_step": round(wall * 1e3 / T, 3), "tokens_per_s": round(gen / wall, 1),
