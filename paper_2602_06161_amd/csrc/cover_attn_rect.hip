@@ -288,16 +288,40 @@ __global__ __launch_bounds__(256) void cover_attn_rect_merge_kernel(const RectPa
   const int b = (int)(bh / p.Hq), h = (int)(bh % p.Hq);
   const float* rec0 = p.ws + (bh * p.n_split * p.Lq + r) * COVER_RECT_RECORD;
   const int64_t sstride = (int64_t)p.Lq * COVER_RECT_RECORD;
-  float M = kInit;
-  for (int s = 0; s < p.n_split; ++s) M = __builtin_fmaxf(M, rec0[s * sstride + kD / 2]);
-  float den = 0.0f, o0 = 0.0f, o1 = 0.0f;
-  for (int s = 0; s < p.n_split; ++s) {
-    const float* rec = rec0 + s * sstride;
-    const float w = rec[kD / 2 + 1] * __builtin_amdgcn_exp2f(rec[kD / 2] - M);
-    const uint32_t pair = ((const uint32_t*)rec)[lane];  // bf16 O of dims 2 lane, 2 lane + 1
-    den += w;
-    o0 = __builtin_fmaf(__uint_as_float(pair << 16), w, o0);
-    o1 = __builtin_fmaf(__uint_as_float(pair & 0xffff0000u), w, o1);
+  // splits in chunks of 8 whose loads are all issued before the first is used; the running
+  // (max, sum, O) is rescaled between chunks
+  constexpr int kChunk = 8;
+  float M = kInit, den = 0.0f, o0 = 0.0f, o1 = 0.0f;
+  for (int s0 = 0; s0 < p.n_split; s0 += kChunk) {
+    float ms[kChunk], ls[kChunk];
+    uint32_t pr[kChunk];
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      ms[u] = kInit;
+      ls[u] = 0.0f;
+      pr[u] = 0u;
+      if (s0 + u < p.n_split) {
+        const float* rec = rec0 + (s0 + u) * sstride;
+        ms[u] = rec[kD / 2];
+        ls[u] = rec[kD / 2 + 1];
+        pr[u] = ((const uint32_t*)rec)[lane];  // bf16 O of dims 2 lane, 2 lane + 1
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) Mn = __builtin_fmaxf(Mn, ms[u]);
+    const float a = __builtin_amdgcn_exp2f(M - Mn);
+    den *= a;
+    o0 *= a;
+    o1 *= a;
+    M = Mn;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const float w = ls[u] * __builtin_amdgcn_exp2f(ms[u] - M);
+      den += w;
+      o0 = __builtin_fmaf(__uint_as_float(pr[u] << 16), w, o0);
+      o1 = __builtin_fmaf(__uint_as_float(pr[u] & 0xffff0000u), w, o1);
+    }
   }
   const float inv = 1.0f / den;
   __bf16* op = p.out + b * p.q_sb + h * p.q_sh + (int64_t)r * p.q_sl + 2 * lane;
