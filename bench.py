@@ -363,7 +363,6 @@ def bench_full_step(args, dev, stream, loop: bool = False) -> int:
     cnt0 = torch.zeros((1, gen), dtype=torch.int32, device=dev)
     seed_idx = torch.from_numpy(seeds.astype(np.int32))[None].to(dev)
     n_seed = torch.tensor([n_seeds], dtype=torch.int32, device=dev)
-    masked_t = torch.from_numpy(masked)[None].to(dev)
 
     def rmsnorm(x):
         xf = x.float()
@@ -421,10 +420,12 @@ def bench_full_step(args, dev, stream, loop: bool = False) -> int:
         # u(j) of the tokens now in place (Sec. 5.3)
         logp, _, _ = cover.cover_token_stats(logits, tok_state[0], want_conf=False,
                                              want_argmax=False, stream=stream)
+        # d_in over M_t, the masked set after the update (Sec. 5.3)
+        masked_now = (tok_state == mask_id).to(torch.uint8)
         k_cur, _ = kv[parity][n_layers - 1]
         k_prev, _ = kv[1 - parity][n_layers - 1]
         d_in, d_out = cover.cover_attn_stats(as4(q_last), as4(k_cur), as4(k_prev), seed_idx, n_seed,
-                                             lse, masked_t, drafted, prompt, stream=stream)
+                                             lse, masked_now, drafted, prompt, stream=stream)
         return cover.cover_select_seeds(logp[None], d_in, d_out, flags, max_seeds, prompt,
                                         stream=stream)
 
@@ -551,12 +552,12 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         logits, lse, q_last = model(ids[:L], parity, seed_idx, attn_n, False)
         logits = logits * args.lm_scale
         _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
-        masked = (tok == mask_id).to(torch.uint8)
         flags, drafted, counts, ff = cover.cover_decode_update(
             tok, am[None], conf[None], seed_idx, n_seed, cnt, mask_id, tau, cap, budget, prompt,
             last_unmask=last, stream=stream)
         logp, _, _ = cover.cover_token_stats(logits, tok[0], want_conf=False, want_argmax=False,
                                              stream=stream)
+        masked = (tok == mask_id).to(torch.uint8)  # M_t, after the update (Sec. 5.3 d_in)
         if args.variant == "wo_seed":
             # confidence drop since drafting: log p at the unmasking minus log p now
             logp_draft = torch.where(drafted == 1, logp[None], logp_draft)
