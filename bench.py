@@ -76,7 +76,14 @@ def main() -> int:
     ap.add_argument("--kernel", choices=["token_stats", "attn_stats"], default=None)
     ap.add_argument("--lm-scale", type=float, default=8.0,
                     help="loop workload: LM-head weights scaled by this (peaked distributions)")
-    ap.add_argument("--max-steps", type=int, default=512, help="loop workload: step budget")
+    ap.add_argument("--max-steps", type=int, default=2048, help="loop workload: step budget")
+    ap.add_argument("--tau", type=float, default=0.9, help="loop workload: drafting threshold")
+    ap.add_argument("--remask-budget", type=int, default=5,
+                    help="loop workload: ReMasks after which a position is no longer a seed")
+    ap.add_argument("--min-draft", type=int, default=1,
+                    help="loop workload: draft at least this many per step (0 = the paper's rule)")
+    ap.add_argument("--block-len", type=int, default=64,
+                    help="loop workload: semi-autoregressive block length (Sec. 6.1: 64 for LLaDA)")
     ap.add_argument("--variant", choices=["cover", "wo_kv", "wo_seed"], default="cover",
                     help="loop workload: COVER, or the ablations of Sec. 6.4 (no KV override; "
                          "confidence-drop seeds)")
@@ -415,7 +422,7 @@ def bench_full_step(args, dev, stream, loop: bool = False) -> int:
         # drafting (at most 15 above 0.9), revision of the seeds, state update, flags
         tok_state, cnt_state = tok0.clone(), cnt0.clone()
         flags, drafted, _ = cover.cover_decode_update(tok_state, am[None], conf[None], seed_idx,
-                                                      n_seed, cnt_state, mask_id, 0.9, cap, 2,
+                                                      n_seed, cnt_state, mask_id, 0.9, cap, 5,
                                                       prompt, stream=stream)
         # u(j) of the tokens now in place (Sec. 5.3)
         logp, _, _ = cover.cover_token_stats(logits, tok_state[0], want_conf=False,
@@ -520,6 +527,13 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     Lemma A.1 bound T >= ceil((L + F) / B) and the unmask-count identity
     sum_t |D_t| = L + #ReMask at completion.
 
+    Semi-autoregressive order (Sec. 6.1): drafting is restricted to the current block of
+    --block-len positions (confidences outside it are NaN: never drafted): the first block
+    that still holds a [MASK], so a block reopened by a ReMask is finished before the next;
+    revision and seed selection cover the whole generated region.  --min-draft
+    (default 1) drafts the most confident masked positions of the block when none passes
+    tau; 0 is the paper's rule, under which a random model can stall.
+
     --variant wo_kv: verification by masking the seeds in the input only (no KV override and
     no diagonal rule: the attention is called without seeds).  --variant wo_seed: the seeds
     are ranked by their confidence drop, log p at drafting minus log p now (same selection
@@ -528,7 +542,7 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     import torch
     from paper_2602_06161_amd import cover
 
-    tau, budget = 0.9, 2
+    tau, budget = args.tau, args.remask_budget  # Sec. 6.1: 0.9 and about 5
     prompt_ids = torch.from_numpy(tokens[:prompt]).to(dev)
     tok = torch.full((1, gen), mask_id, dtype=torch.int32, device=dev)
     cnt = torch.zeros((1, gen), dtype=torch.int32, device=dev)
@@ -540,6 +554,9 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     logp_draft = torch.zeros((1, gen), dtype=torch.float32, device=dev)
     zeros = torch.zeros((1, gen), dtype=torch.float32, device=dev)
     tot = np.zeros(6, np.int64)  # |D|, kept, replaced, remasked, (unused), flip-flops
+    blk = max(1, min(args.block_len, gen))
+    pos = torch.arange(gen, device=dev)
+    cur = 0  # current block
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     T, done, idle = 0, False, 0
@@ -552,9 +569,11 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         logits, lse, q_last = model(ids[:L], parity, seed_idx, attn_n, False)
         logits = logits * args.lm_scale
         _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
+        in_blk = (pos >= cur * blk) & (pos < (cur + 1) * blk)
+        conf_blk = torch.where(in_blk, conf, torch.full_like(conf, float("nan")))  # never drafted
         flags, drafted, counts, ff = cover.cover_decode_update(
-            tok, am[None], conf[None], seed_idx, n_seed, cnt, mask_id, tau, cap, budget, prompt,
-            last_unmask=last, stream=stream)
+            tok, am[None], conf_blk[None], seed_idx, n_seed, cnt, mask_id, tau, cap, budget,
+            prompt, last_unmask=last, min_draft=args.min_draft, stream=stream)
         logp, _, _ = cover.cover_token_stats(logits, tok[0], want_conf=False, want_argmax=False,
                                              stream=stream)
         masked = (tok == mask_id).to(torch.uint8)  # M_t, after the update (Sec. 5.3 d_in)
@@ -578,6 +597,8 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         tot[5] += int(ff[0].item())
         T += 1
         done = c[4] == 0
+        if not done:  # the first block that still holds a [MASK] (a ReMask can reopen one)
+            cur = int(torch.argmax((tok[0] == mask_id).to(torch.int32)).item()) // blk
         idle = idle + 1 if c[0] == 0 and c[3] == 0 else 0  # no draft and no ReMask: no progress
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -587,7 +608,9 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     print(json.dumps({
         "workload": f"{args.variant} decoding loop, random-init LLaDA-8B-shaped model (32 "
                     f"layers), B=1, prompt {prompt} + block {gen} from all [MASK], tau {tau}, cap {cap}, "
-                    f"ReMask budget {budget}, {max_seeds} seeds max, LM head x{args.lm_scale}",
+                    f"ReMask budget {budget}, {max_seeds} seeds max, blocks of {blk}, "
+                    f"min_draft {args.min_draft}, "
+                    f"LM head x{args.lm_scale}",
         "steps": T, "terminated": bool(done), "stalled": idle >= 32, "wall_s": round(wall, 3),
         "ms_per_step": round(wall * 1e3 / T, 3), "tokens_per_s": round(gen / wall, 1),
         "drafted": int(tot[0]), "kept": int(tot[1]), "replaced": int(tot[2]),

@@ -284,6 +284,10 @@ cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_li
  *   draft_cap      most positions drafted per row and step (>= 0)
  *   remask_budget  ReMasks after which a position is no longer selectable as a seed
  *   tau            confidence threshold (not NaN), used for drafting and for Replace
+ *   min_draft      0 <= min_draft <= draft_cap; 0 is the paper's rule.  Otherwise, when fewer
+ *                  than min_draft masked positions pass tau, the min_draft most confident
+ *                  masked positions (same order; NaN confidences never drafted) are drafted
+ *                  instead, so a decoding loop always progresses (not in the paper)
  */
 typedef struct {
   int32_t B, Lr;
@@ -293,6 +297,7 @@ typedef struct {
   int32_t draft_cap;
   int32_t remask_budget;
   float tau;
+  int32_t min_draft;
 } cover_update_desc;
 
 /*

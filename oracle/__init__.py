@@ -222,7 +222,7 @@ def attn_stats(q, k_live, k_cache, seed_idx, n_seed, r0, masked, drafted, scale=
 
 
 def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id, tau, cap,
-                  remask_budget, pos_offset=0, last_unmask=None):
+                  remask_budget, pos_offset=0, last_unmask=None, min_draft=0):
     """One decoding step's state update over a region of Lr positions (absolute position =
     pos_offset + region index), for each batch row:
 
@@ -238,6 +238,9 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
     next selection's flags (Sec. 5.3, exclusion): bit 0 = unmasked after the update; bit 1 =
       i was a seed this step, or remask_count_i >= remask_budget.
 
+    min_draft (not in the paper; 0 keeps its rule): when fewer than min_draft masked positions
+      pass tau, the min_draft most confident masked positions (same order) are drafted
+      instead, so that a decoding loop always progresses.
     flip-flops (Sec. 4, Definition): with last_unmask given (the token of each position's most
       recent [MASK] -> token transition, -1 if none yet), a drafted position whose new token
       equals its last_unmask entry is a flip-flop event; every drafted position then records
@@ -271,6 +274,10 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
         cand = [i for i in range(Lr) if tok[b, i] == mask_id and c[b, i] > t32]
         cand.sort(key=lambda i: (-float(c[b, i]), i))
         D = cand[:max(0, int(cap))]
+        if len(cand) < min_draft:
+            masked = [i for i in range(Lr) if tok[b, i] == mask_id and not np.isnan(c[b, i])]
+            masked.sort(key=lambda i: (-float(c[b, i]), i))
+            D = masked[:min_draft]
         # revision of the seeds
         kept = replaced = 0
         R = []

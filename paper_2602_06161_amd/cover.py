@@ -55,7 +55,7 @@ class UpdateDesc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("Lr", ctypes.c_int32), ("max_seeds", ctypes.c_int32),
                 ("pos_offset", ctypes.c_int32), ("mask_id", ctypes.c_int32),
                 ("draft_cap", ctypes.c_int32), ("remask_budget", ctypes.c_int32),
-                ("tau", ctypes.c_float)]
+                ("tau", ctypes.c_float), ("min_draft", ctypes.c_int32)]
 
 
 class RectDesc(ctypes.Structure):
@@ -261,7 +261,7 @@ def cover_select_seeds(logp, d_in, d_out, flags, max_seeds: int, pos_offset: int
 def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id: int,
                         tau: float, draft_cap: int, remask_budget: int, pos_offset: int = 0,
                         flags=None, drafted=None, counts=None, want_outputs: bool = True,
-                        last_unmask=None, flipflops=None, stream=None):
+                        last_unmask=None, flipflops=None, min_draft: int = 0, stream=None):
     """One step's decoding-state update, in place on tokens and remask_count (int32 [B,Lr]);
     argmax int32 / conf fp32 [B,Lr]; seed_idx int32 [B,max_seeds], n_seed int32 [B] (may be
     None: no seeds).  Returns (flags uint8, drafted uint8, counts int32 [B,5]), allocated
@@ -293,7 +293,8 @@ def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, ma
                              "last_unmask int32 [B,Lr], flipflops int32 [B]")
     if last_unmask is not None and flipflops is None:
         flipflops = torch.empty((B,), device=dev, dtype=torch.int32)
-    desc = UpdateDesc(B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget, tau)
+    desc = UpdateDesc(B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget, tau,
+                      min_draft)
     st = lib().cover_decode_update(_ptr(tokens), _ptr(argmax), _ptr(conf),
                                    _ptr(seed_idx) if max_seeds else None,
                                    _ptr(n_seed) if max_seeds else None, _ptr(remask_count),

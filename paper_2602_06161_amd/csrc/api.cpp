@@ -238,6 +238,7 @@ cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const f
   if (!desc) return COVER_ERR_INVALID;
   const cover_update_desc& D = *desc;
   if (D.B < 0 || D.Lr < 0 || D.max_seeds < 0 || D.draft_cap < 0) return COVER_ERR_INVALID;
+  if (D.min_draft < 0 || D.min_draft > D.draft_cap) return COVER_ERR_INVALID;
   if (!(D.tau == D.tau)) return COVER_ERR_INVALID;  // NaN
   if (D.Lr > COVER_MAX_LR) return COVER_ERR_UNSUPPORTED;
   if (D.B == 0) return COVER_OK;
@@ -260,7 +261,7 @@ cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const f
   a.flipflops = flipflops;
   a.B = D.B; a.Lr = D.Lr; a.max_seeds = D.max_seeds; a.pos_offset = D.pos_offset;
   a.mask_id = D.mask_id; a.draft_cap = D.draft_cap; a.remask_budget = D.remask_budget;
-  a.tau = D.tau;
+  a.tau = D.tau; a.min_draft = D.min_draft;
   return hip_status(cover::launch_decode_update(a, stream));
 }
 

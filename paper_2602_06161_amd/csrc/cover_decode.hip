@@ -11,6 +11,8 @@
 //      confidence mapped to an order-preserving unsigned integer in the high half, the
 //      bitwise complement of the position in the low half.  Keys are distinct and their
 //      order is (confidence descending, position ascending);
+//      With min_draft > 0 and fewer candidates than that, every masked position with a
+//      confidence becomes a candidate and min_draft of them are drafted instead;
 //   3. if more candidates qualify than the cap allows, the cap-th largest key is found by a
 //      most-significant-digit radix select (8-bit digits, LDS histogram, one wave scans the
 //      256 bins), which stops at the first digit whose bucket is taken whole; the drafts are
@@ -43,7 +45,7 @@ struct UpdParams {
   int32_t* counts;
   int32_t* last_unmask;
   int32_t* flipflops;
-  int Lr, per, max_seeds, pos_offset, mask_id, cap, budget;
+  int Lr, per, max_seeds, pos_offset, mask_id, cap, budget, min_draft;
   float tau;
 };
 
@@ -63,14 +65,15 @@ __device__ __forceinline__ int wave_sum(int v) {
 __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdParams p) {
   __shared__ uint32_t seedbits[COVER_MAX_LR / 32];
   __shared__ uint32_t hist[256];
-  __shared__ int sums[7];  // candidates, |D|, kept, replaced, remasked, masked after, flip-flops
+  // candidates, |D|, kept, replaced, remasked, masked after, flip-flops, forced candidates
+  __shared__ int sums[8];
   __shared__ uint64_t s_prefix;
   __shared__ int s_need, s_done, s_shift;
 
   const int b = blockIdx.x, tid = threadIdx.x, nth = blockDim.x, lane = tid & 63;
   const int64_t base = (int64_t)b * p.Lr;
   for (int w = tid; w < (p.Lr + 31) / 32; w += nth) seedbits[w] = 0u;
-  if (tid < 7) sums[tid] = 0;
+  if (tid < 8) sums[tid] = 0;
   __syncthreads();
 
   // 1. per-position inputs, and the seed bitmap
@@ -109,13 +112,32 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   if (lane == 0 && nc) atomicAdd(&sums[0], nc);
   __syncthreads();
 
-  // 3. drafts: every candidate, or the cap largest keys
+  int target = p.cap, total = sums[0];
+  if (total < p.min_draft) {  // too few above tau: the min_draft most confident masked ones
+    cand = 0;
+#pragma unroll
+    for (int m = 0; m < kMaxPer; ++m) {
+      const int j = tid + m * nth;
+      key[m] = 0;
+      if (m < p.per && j < p.Lr && tok[m] == p.mask_id && cf[m] == cf[m]) {
+        cand |= 1u << m;
+        key[m] = ((uint64_t)ordered(cf[m]) << 32) | (uint32_t)~(uint32_t)j;
+      }
+    }
+    const int n2 = wave_sum(__builtin_popcount(cand));
+    if (lane == 0 && n2) atomicAdd(&sums[7], n2);
+    __syncthreads();
+    target = p.min_draft;
+    total = sums[7];
+  }
+
+  // 3. drafts: every candidate, or the `target` largest keys
   uint64_t keep_mask = 0, prefix = 0;  // drafted <=> candidate and (key & keep_mask) >= prefix
-  bool none = p.cap <= 0;
-  if (!none && sums[0] > p.cap) {
+  bool none = target <= 0;
+  if (!none && total > target) {
     if (tid == 0) {
       s_prefix = 0;
-      s_need = p.cap;  // rank, from the top, of the key still to be located
+      s_need = target;  // rank, from the top, of the key still to be located
       s_done = 0;
     }
     for (int shift = 56; shift >= 0; shift -= 8) {
@@ -226,7 +248,7 @@ hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream) {
   p.flags = a.flags; p.drafted = a.drafted; p.counts = a.counts;
   p.last_unmask = a.last_unmask; p.flipflops = a.flipflops;
   p.Lr = a.Lr; p.max_seeds = a.max_seeds; p.pos_offset = a.pos_offset; p.mask_id = a.mask_id;
-  p.cap = a.draft_cap; p.budget = a.remask_budget; p.tau = a.tau;
+  p.cap = a.draft_cap; p.budget = a.remask_budget; p.tau = a.tau; p.min_draft = a.min_draft;
   int nth = ((a.Lr + 63) / 64) * 64;
   if (nth < 64) nth = 64;
   if (nth > kMaxThreads) nth = kMaxThreads;

@@ -90,6 +90,7 @@ struct UpdateArgs {
   int32_t* flipflops;    // may be null (always null when last_unmask is)
   int32_t B, Lr, max_seeds, pos_offset, mask_id, draft_cap, remask_budget;
   float tau;
+  int32_t min_draft;
 };
 
 hipError_t launch_attn_bf16(const AttnArgs& a, hipStream_t stream);     // bf16, d = 64

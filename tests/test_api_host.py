@@ -189,6 +189,8 @@ def test_decode_update_rejects_bad_arguments():
     assert _upd(d(max_seeds=-1)) == cover.COVER_ERR_INVALID
     assert _upd(d(draft_cap=-1)) == cover.COVER_ERR_INVALID
     assert _upd(d(tau=float("nan"))) == cover.COVER_ERR_INVALID
+    assert _upd(d(min_draft=-1)) == cover.COVER_ERR_INVALID
+    assert _upd(d(min_draft=16)) == cover.COVER_ERR_INVALID          # above draft_cap
     assert _upd(d(Lr=cover.COVER_MAX_LR + 1)) == cover.COVER_ERR_UNSUPPORTED
     assert _upd(d(), tok=None) == cover.COVER_ERR_INVALID
     assert _upd(d(), tok=FAKE + 2) == cover.COVER_ERR_INVALID

@@ -14,20 +14,21 @@ from paper_2602_06161_amd import cover, synth
 pytestmark = pytest.mark.gpu
 
 
-def _both(a, tau, cap, budget, seeds=True, last=None):
+def _both(a, tau, cap, budget, seeds=True, last=None, min_draft=0):
     announce(f"decode update B{a['tokens'].shape[0]} Lr{a['tokens'].shape[1]} tau{tau} cap{cap}")
     si = a["seed_idx"] if seeds else np.zeros((a["tokens"].shape[0], 0), np.int32)
     ns = a["n_seed"] if seeds else np.zeros(a["tokens"].shape[0], np.int32)
     exp = oracle.decode_update(a["tokens"].numpy(), a["argmax"].numpy(), a["conf"].numpy(),
                                np.asarray(si), np.asarray(ns), a["remask_count"].numpy(),
                                a["mask_id"], tau, cap, budget, a["pos_offset"],
+                               min_draft=min_draft,
                                **({} if last is None else {"last_unmask": last}))
     tok, cnt = a["tokens"].cuda(), a["remask_count"].cuda()
     lt = None if last is None else torch.from_numpy(np.ascontiguousarray(last)).cuda()
     r = cover.cover_decode_update(
         tok, a["argmax"].cuda(), a["conf"].cuda(), a["seed_idx"].cuda() if seeds else None,
         a["n_seed"].cuda() if seeds else None, cnt, a["mask_id"], tau, cap, budget,
-        a["pos_offset"], last_unmask=lt)
+        a["pos_offset"], last_unmask=lt, min_draft=min_draft)
     torch.cuda.synchronize()
     got = (tok.cpu().numpy(), cnt.cpu().numpy(), r[0].cpu().numpy(), r[1].cpu().numpy(),
            r[2].cpu().numpy())
@@ -108,3 +109,11 @@ def test_chained_steps_keep_state():
             a["seed_idx"][b, :ok.size] = torch.from_numpy(768 + ok.astype(np.int32))
             a["n_seed"][b] = ok.size
     assert total_ff > 0
+
+
+@pytest.mark.parametrize("tau,min_draft,levels", [(0.999, 1, 0), (0.999, 15, 3), (0.5, 4, 0),
+                                                  (2.0, 15, 0)])
+def test_min_draft(tau, min_draft, levels):
+    # forced drafting when too few pass tau (ties among few levels), unchanged otherwise
+    a = synth.update_inputs(2, 700, seed=min_draft, conf_levels=levels)
+    _both(a, tau, 15, 5, min_draft=min_draft)

@@ -147,6 +147,27 @@ def _history_ok(fn, seed, steps=40, Lr=48):
     return F == F_def and n_d == sum(len(h) for h in hist) and F > 0
 
 
+def test_min_draft_forces_progress_only_when_needed():
+    # nothing above tau: the two most confident masked positions are drafted (ties by position)
+    tok = np.array([[9, 9, 9, 1, 9]], np.int32)
+    am = np.array([[4, 5, 6, 1, 7]], np.int32)
+    conf = np.array([[0.3, 0.6, 0.6, 0.99, 0.1]], np.float32)
+    none = (np.zeros((1, 0), np.int32), np.zeros(1, np.int32), np.zeros((1, 5), np.int32))
+    r = oracle.decode_update(tok, am, conf, none[0], none[1], none[2], 9, 0.9, 15, 5, 0,
+                             min_draft=2)
+    assert r[3][0].tolist() == [0, 1, 1, 0, 0] and r[0][0].tolist() == [9, 5, 6, 1, 9]
+    # enough above tau: min_draft changes nothing; 0 keeps the paper's rule
+    conf2 = np.array([[0.95, 0.6, 0.6, 0.99, 0.97]], np.float32)
+    a = oracle.decode_update(tok, am, conf2, *none, 9, 0.9, 15, 5, 0, min_draft=2)
+    b = oracle.decode_update(tok, am, conf2, *none, 9, 0.9, 15, 5, 0)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    c = oracle.decode_update(tok, am, conf, *none, 9, 0.9, 15, 5, 0)
+    assert not c[3].any()
+    # fewer masked positions than min_draft: all of them
+    d = oracle.decode_update(tok, am, conf, *none, 9, 0.9, 15, 5, 0, min_draft=10)
+    assert d[3][0].tolist() == [1, 1, 1, 0, 1]
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_flip_flops_match_the_definition_over_a_history(seed):
     assert _history_ok(oracle.decode_update, seed)
