@@ -308,3 +308,63 @@ def decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, mask_id,
     if last is not None:
         out = out + (last.astype(np.int32), ff.astype(np.int32))
     return out
+
+
+# ---- temperature sampling of the draft tokens (stochastic decoding, App. "Robustness under
+# stochastic decoding") ----------------------------------------------------------------------
+
+_PHILOX_M = (0xD2511F53, 0xCD9E8D57)  # Philox4x32 multipliers (Salmon et al., SC 2011)
+_PHILOX_W = (0x9E3779B9, 0xBB67AE85)  # Weyl key increments
+_U32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(c0, c1, c2, c3, k0, k1):
+    """The Philox4x32-10 counter-based generator as published (Salmon, Moraes, Dror, Shaw,
+    "Parallel random numbers: as easy as 1, 2, 3", SC 2011): ten rounds of two 32x32 -> 64-bit
+    multiplications whose halves are mixed with the other two counter words and the key, the
+    key advanced by the Weyl constants between rounds.  Arguments: arrays (or scalars) of
+    32-bit values; returns the four 32-bit output words as uint64 arrays."""
+    c = [np.asarray(x, dtype=np.uint64) & _U32 for x in (c0, c1, c2, c3)]
+    k0 = np.asarray(k0, dtype=np.uint64) & _U32
+    k1 = np.asarray(k1, dtype=np.uint64) & _U32
+    for r in range(10):
+        if r:
+            k0 = (k0 + np.uint64(_PHILOX_W[0])) & _U32
+            k1 = (k1 + np.uint64(_PHILOX_W[1])) & _U32
+        p0 = np.uint64(_PHILOX_M[0]) * c[0]
+        p1 = np.uint64(_PHILOX_M[1]) * c[2]
+        hi0, lo0 = p0 >> np.uint64(32), p0 & _U32
+        hi1, lo1 = p1 >> np.uint64(32), p1 & _U32
+        c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
+    return c
+
+
+def sample_uniforms(R, V, seed, step):
+    """u[r, v] in (0, 1): word v % 4 of Philox4x32-10 with counter (v // 4, r, step, 0) and
+    key (seed mod 2^32, seed >> 32), mapped as ((w >> 9) + 1/2) 2^-23 (exact in fp32)."""
+    v = np.arange(V, dtype=np.uint64)
+    r = np.arange(R, dtype=np.uint64)[:, None]
+    words = philox4x32_10(v[None, :] // np.uint64(4), r, np.uint64(step), np.uint64(0),
+                          np.uint64(seed & 0xFFFFFFFF), np.uint64((seed >> 32) & 0xFFFFFFFF))
+    w = np.choose((v % np.uint64(4)).astype(np.int64)[None, :].repeat(R, 0),
+                  [np.broadcast_to(x, (R, V)) for x in words])
+    return ((w >> np.uint64(9)).astype(np.float64) + 0.5) * 2.0 ** -23
+
+
+def token_sample(logits, temperature, seed, step):
+    """Temperature sampling per row of logits [R, V] (the stochastic drafting the paper tests
+    at T in {0.1, 0.2, 0.3}) by the Gumbel-max construction: token = argmax_v (x_v / T + g_v)
+    with g_v = -ln(-ln u_v) standard Gumbel noise from sample_uniforms (smallest v on ties),
+    which draws v with probability softmax(x / T)_v; its probability p = softmax(x / T) at the
+    token is the confidence the drafting rule compares with tau.  fp64.  Returns (token int32
+    [R], p [R], y [R, V] the perturbed scores)."""
+    x = np.asarray(logits, dtype=np.float64)
+    R, V = x.shape
+    u = sample_uniforms(R, V, seed, step)
+    y = x / temperature - np.log(-np.log(u))
+    tok = np.argmax(y, axis=1)
+    z = x / temperature
+    zm = z.max(axis=1, keepdims=True)
+    lse = zm[:, 0] + np.log(np.exp(z - zm).sum(axis=1))
+    p = np.exp(z[np.arange(R), tok] - lse)
+    return tok.astype(np.int32), p, y
