@@ -80,6 +80,8 @@ def main() -> int:
     ap.add_argument("--tau", type=float, default=0.9, help="loop workload: drafting threshold")
     ap.add_argument("--remask-budget", type=int, default=5,
                     help="loop workload: ReMasks after which a position is no longer a seed")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="loop workload: sampling temperature of the predictions (0 = argmax)")
     ap.add_argument("--min-draft", type=int, default=1,
                     help="loop workload: draft at least this many per step (0 = the paper's rule)")
     ap.add_argument("--block-len", type=int, default=64,
@@ -532,7 +534,9 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
     that still holds a [MASK], so a block reopened by a ReMask is finished before the next;
     revision and seed selection cover the whole generated region.  --min-draft
     (default 1) drafts the most confident masked positions of the block when none passes
-    tau; 0 is the paper's rule, under which a random model can stall.
+    tau; 0 is the paper's rule, under which a random model can stall.  --temperature T > 0
+    replaces the argmax predictions and their probabilities by temperature samples
+    (cover_token_sample, seeded by --seed and the step index), for drafting and revision.
 
     --variant wo_kv: verification by masking the seeds in the input only (no KV override and
     no diagonal rule: the attention is called without seeds).  --variant wo_seed: the seeds
@@ -568,7 +572,11 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         attn_n = no_seeds if args.variant == "wo_kv" else n_seed
         logits, lse, q_last = model(ids[:L], parity, seed_idx, attn_n, False)
         logits = logits * args.lm_scale
-        _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
+        if args.temperature > 0:  # stochastic decoding: sampled tokens and their probabilities
+            am, conf = cover.cover_token_sample(logits, args.temperature, args.seed, T,
+                                                stream=stream)
+        else:
+            _, conf, am = cover.cover_token_stats(logits, want_logp=False, stream=stream)
         in_blk = (pos >= cur * blk) & (pos < (cur + 1) * blk)
         conf_blk = torch.where(in_blk, conf, torch.full_like(conf, float("nan")))  # never drafted
         flags, drafted, counts, ff = cover.cover_decode_update(
@@ -609,7 +617,7 @@ def decode_loop(args, dev, stream, model, emb, lm_head, kv, as4, tokens, L, prom
         "workload": f"{args.variant} decoding loop, random-init LLaDA-8B-shaped model (32 "
                     f"layers), B=1, prompt {prompt} + block {gen} from all [MASK], tau {tau}, cap {cap}, "
                     f"ReMask budget {budget}, {max_seeds} seeds max, blocks of {blk}, "
-                    f"min_draft {args.min_draft}, "
+                    f"min_draft {args.min_draft}, temperature {args.temperature}, "
                     f"LM head x{args.lm_scale}",
         "steps": T, "terminated": bool(done), "stalled": idle >= 32, "wall_s": round(wall, 3),
         "ms_per_step": round(wall * 1e3 / T, 3), "tokens_per_s": round(gen / wall, 1),

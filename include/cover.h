@@ -192,6 +192,23 @@ cover_status cover_token_stats(const void* logits, const int32_t* tokens,
                                const cover_token_desc* desc, hipStream_t stream);
 
 /*
+ * cover_token_sample -- temperature sampling of the draft tokens (the stochastic decoding of
+ * the paper's appendix on robustness): per row r of logits (same description and layout
+ * rules as cover_token_stats),
+ *   token[r] = argmax_v (x_v / T + g_v), g_v = -ln(-ln u_v) (Gumbel-max: a draw from
+ *              softmax(x / T); the smallest v on ties)
+ *   prob[r]  = softmax(x / T) at token[r] (the confidence compared with the drafting
+ *              threshold; may be NULL)
+ * u_v = ((w >> 9) + 1/2) 2^-23 with w word v % 4 of Philox4x32-10 (Salmon et al., SC 2011)
+ * at counter (v / 4, r, step, 0) and key (seed mod 2^32, seed >> 32): a fixed function of
+ * (seed, step, row, token), reproducible across launches and devices.  Arithmetic in fp32.
+ * temperature: > 0 and finite.  token int32 [R], prob fp32 [R]: device outputs.
+ */
+cover_status cover_token_sample(const void* logits, float temperature, uint64_t seed, uint32_t step,
+                                int32_t* token, float* prob, const cover_token_desc* desc,
+                                hipStream_t stream);
+
+/*
  * Attention-mass description: the attention problem of cover_attn_fwd (same fields and
  * stride rules; bf16 only) plus the response region [r0, r0 + Lr).
  *   r0, Lr      0 <= r0, 1 <= Lr, r0 + Lr <= L (Lr == 0 is a no-op)

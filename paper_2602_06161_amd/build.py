@@ -38,6 +38,7 @@ SOURCES = {
     "cover_decode.hip": [],
     "cover_select.hip": ["-ffp-contract=off"],  # the selection is bit-exact fp64
     "cover_stats.hip": [],
+    "cover_sample.hip": [],
 }
 
 

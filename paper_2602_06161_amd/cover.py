@@ -21,7 +21,8 @@ COVER_MAX_LR = 16384
 COVER_RECT_RECORD = 68
 
 EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_debug_status", "cover_decode_update",
-            "cover_select_seeds", "cover_status_str", "cover_token_stats", "cover_version")
+            "cover_select_seeds", "cover_status_str", "cover_token_sample", "cover_token_stats",
+            "cover_version")
 # status bits of the contract checks that COVER_DEBUG=1 enables (cover_debug_status)
 COVER_DEBUG_SEED_COUNT, COVER_DEBUG_SEED_RANGE, COVER_DEBUG_SEED_DUPLICATE = 1, 2, 4
 COVER_DEBUG_SELECT_NONFINITE, COVER_DEBUG_SELECT_NEGATIVE = 8, 16
@@ -95,6 +96,9 @@ def lib():
                                           ctypes.POINTER(UpdateDesc), P]
         L.cover_decode_update.restype = ctypes.c_int
         L.cover_token_stats.restype = ctypes.c_int
+        L.cover_token_sample.argtypes = [P, ctypes.c_float, ctypes.c_uint64, ctypes.c_uint32, P, P,
+                                         ctypes.POINTER(TokenDesc), P]
+        L.cover_token_sample.restype = ctypes.c_int
         L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
         L.cover_attn_stats.restype = ctypes.c_int
         L.cover_status_str.argtypes = [ctypes.c_int]
@@ -305,6 +309,26 @@ def cover_decode_update(tokens, argmax, conf, seed_idx, n_seed, remask_count, ma
     if last_unmask is not None:
         return flags, drafted, counts, flipflops
     return flags, drafted, counts
+
+
+def cover_token_sample(logits, temperature: float, seed: int, step: int, want_prob: bool = True,
+                       stream=None):
+    """Temperature sampling per row of logits [R, V] (bf16 or fp32, last dimension
+    contiguous, row stride a multiple of 16 bytes).  Returns (token int32 [R], prob fp32 [R]
+    or None)."""
+    R, V = logits.shape
+    dt = {torch.float32: COVER_F32, torch.bfloat16: COVER_BF16}.get(logits.dtype)
+    if dt is None or logits.stride(-1) != 1:
+        raise ValueError("logits must be bf16 or fp32 with a contiguous last dimension")
+    token = torch.empty(R, device=logits.device, dtype=torch.int32)
+    prob = torch.empty(R, device=logits.device, dtype=torch.float32) if want_prob else None
+    desc = TokenDesc(R, V, dt, logits.stride(0))
+    st = lib().cover_token_sample(_ptr(logits), float(temperature), int(seed) & (2**64 - 1),
+                                  int(step) & 0xFFFFFFFF, _ptr(token), _ptr(prob),
+                                  ctypes.byref(desc), _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_token_sample")
+    return token, prob
 
 
 def cover_token_stats(logits, tokens=None, want_logp: bool = True, want_conf: bool = True,

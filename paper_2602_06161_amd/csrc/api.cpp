@@ -134,6 +134,26 @@ cover_status cover_token_stats(const void* logits, const int32_t* tokens,
   return hip_status(cover::launch_token_stats(a, stream));
 }
 
+cover_status cover_token_sample(const void* logits, float temperature, uint64_t seed, uint32_t step,
+                                int32_t* token, float* prob, const cover_token_desc* desc,
+                                hipStream_t stream) {
+  if (!desc) return COVER_ERR_INVALID;
+  const cover_token_desc& D = *desc;
+  if (D.R < 0 || D.V < 1 || D.row_stride < D.V) return COVER_ERR_INVALID;
+  if (D.dtype != COVER_F32 && D.dtype != COVER_BF16) return COVER_ERR_INVALID;
+  const int64_t esz = D.dtype == COVER_BF16 ? 2 : 4;
+  if ((D.row_stride * esz) % 16 != 0) return COVER_ERR_INVALID;
+  if (!(temperature > 0.0f) || isinf(temperature)) return COVER_ERR_INVALID;
+  if (D.R == 0) return COVER_OK;
+  if (!logits || !aligned(logits, 16) || !token || !aligned(token, 4)) return COVER_ERR_INVALID;
+  if (prob && !aligned(prob, 4)) return COVER_ERR_INVALID;
+  cover::SampleArgs a;
+  a.logits = logits; a.token = token; a.prob = prob;
+  a.R = D.R; a.V = D.V; a.bf16 = D.dtype == COVER_BF16; a.row_stride = D.row_stride;
+  a.temperature = temperature; a.seed = seed; a.step = step;
+  return hip_status(cover::launch_token_sample(a, stream));
+}
+
 cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
                               const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
                               const uint8_t* masked, const uint8_t* drafted,

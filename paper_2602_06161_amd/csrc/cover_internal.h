@@ -43,6 +43,18 @@ struct TokenArgs {
   int64_t row_stride;     // elements
 };
 
+struct SampleArgs {
+  const void* logits;
+  int32_t* token;
+  float* prob;  // may be null
+  int32_t R, V;
+  int bf16;
+  int64_t row_stride;  // elements
+  float temperature;   // > 0
+  uint64_t seed;
+  uint32_t step;
+};
+
 struct StatsArgs {
   const void* q;
   const void* k_live;
@@ -98,6 +110,7 @@ hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream);  // bf16,
 hipError_t launch_attn_f32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
+hipError_t launch_token_sample(const SampleArgs& a, hipStream_t stream);
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
 hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream);
 hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream);  // bf16, d = 128

@@ -1,0 +1,177 @@
+// Temperature sampling of the draft tokens on gfx950 (the stochastic decoding the paper tests
+// in its appendix on robustness, T in {0.1, 0.2, 0.3}).
+//
+// Per row of logits x (one workgroup of 1024 threads per row, one pass over the row):
+//   token = argmax_v (x_v / T + g_v),  g_v = -ln(-ln u_v)   (Gumbel-max: token ~ softmax(x/T))
+//   p     = softmax(x / T) at the token (the confidence the drafting threshold compares)
+// u_v is word v % 4 of Philox4x32-10 (Salmon et al., SC 2011) at counter (v / 4, row, step, 0)
+// and key (seed mod 2^32, seed / 2^32), mapped to ((w >> 9) + 1/2) 2^-23, so every (row,
+// token, step) has its own fixed random number whatever the launch shape.  Each thread keeps
+// the best perturbed score with its index and logit, and an online (max, sum of exp) of x/T;
+// the workgroup merges them (ties: smaller index).  HBM-bound in principle (one read of the
+// logits); the generator costs about 15 integer operations per token.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cover.h"
+#include "cover_internal.h"
+
+namespace cover {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+
+constexpr int kThreads = 1024;
+constexpr float kLog2e = 1.44269504088896341f;
+constexpr float kLn2 = 0.693147180559945309f;
+
+struct SampleParams {
+  const char* logits;
+  int32_t* token;
+  float* prob;
+  int64_t row_stride_bytes;
+  int V, bf16;
+  float inv_t;  // 1 / T
+  uint32_t k0, k1, step;
+};
+
+// Philox4x32-10: ten rounds; each multiplies counter words 0 and 2 by the two round
+// constants and mixes the 64-bit products' halves with words 1 and 3 and the key, which is
+// advanced by the Weyl constants between rounds.
+__device__ __forceinline__ u32x4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                        uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return u32x4{c0, c1, c2, c3};
+}
+
+// standard Gumbel noise from one 32-bit word
+__device__ __forceinline__ float gumbel(uint32_t w) {
+  const float u = ((float)(w >> 9) + 0.5f) * 1.1920928955078125e-7f;  // 2^-23
+  const float nl = -__builtin_amdgcn_logf(u) * kLn2;                 // -ln u > 0
+  return -__builtin_amdgcn_logf(nl) * kLn2;
+}
+
+struct Acc {
+  float y;   // best perturbed score
+  int i;     // its index
+  float z;   // its x / T
+  float m;   // max of x / T
+  float s;   // sum of exp(x / T - m)
+};
+
+__device__ __forceinline__ void add(Acc& a, float z, float g, int v) {
+  const float y = z + g;
+  if (y > a.y || (y == a.y && v < a.i)) {
+    a.y = y;
+    a.i = v;
+    a.z = z;
+  }
+  if (z > a.m) {
+    a.s = a.s * __builtin_amdgcn_exp2f((a.m - z) * kLog2e);
+    a.m = z;
+  }
+  a.s += __builtin_amdgcn_exp2f((z - a.m) * kLog2e);
+}
+
+__device__ __forceinline__ Acc merge(Acc a, const Acc& b) {
+  if (b.y > a.y || (b.y == a.y && b.i < a.i)) {
+    a.y = b.y;
+    a.i = b.i;
+    a.z = b.z;
+  }
+  const float m = fmaxf(a.m, b.m);
+  const float sa = a.s == 0.0f ? 0.0f : a.s * __builtin_amdgcn_exp2f((a.m - m) * kLog2e);
+  const float sb = b.s == 0.0f ? 0.0f : b.s * __builtin_amdgcn_exp2f((b.m - m) * kLog2e);
+  a.m = m;
+  a.s = sa + sb;
+  return a;
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const SampleParams p) {
+  __shared__ Acc red[kThreads / 64];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const char* row = p.logits + (int64_t)r * p.row_stride_bytes;
+  const int per = p.bf16 ? 8 : 4;  // elements per 16-byte chunk
+  const int nfull = p.V / per;
+  Acc acc = {-INFINITY, 0x7fffffff, 0.0f, -INFINITY, 0.0f};
+  for (int c = tid; c < nfull; c += kThreads) {
+    const u32x4 raw = *(gu32x4*)((__attribute__((address_space(1))) const char*)row + (int64_t)c * 16);
+    if (p.bf16) {
+      const u32x4 w0 = philox(2u * c, r, p.step, 0u, p.k0, p.k1);
+      const u32x4 w1 = philox(2u * c + 1u, r, p.step, 0u, p.k0, p.k1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = 8 * c + 2 * e;
+        add(acc, bf_lo(raw[e]) * p.inv_t, gumbel(e < 2 ? w0[2 * e] : w1[2 * e - 4]), v);
+        add(acc, bf_hi(raw[e]) * p.inv_t, gumbel(e < 2 ? w0[2 * e + 1] : w1[2 * e - 3]), v + 1);
+      }
+    } else {
+      const u32x4 w = philox((uint32_t)c, r, p.step, 0u, p.k0, p.k1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) add(acc, __uint_as_float(raw[e]) * p.inv_t, gumbel(w[e]), 4 * c + e);
+    }
+  }
+  // the tail: one element per thread, read at its own width
+  if (tid < p.V - nfull * per) {
+    const int v = nfull * per + tid;
+    const float x = p.bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
+    const u32x4 w = philox((uint32_t)(v >> 2), r, p.step, 0u, p.k0, p.k1);
+    add(acc, x * p.inv_t, gumbel(w[v & 3]), v);
+  }
+  // merge: across the wave, then the waves
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Acc b;
+    b.y = __shfl_xor(acc.y, o);
+    b.i = __shfl_xor(acc.i, o);
+    b.z = __shfl_xor(acc.z, o);
+    b.m = __shfl_xor(acc.m, o);
+    b.s = __shfl_xor(acc.s, o);
+    acc = merge(acc, b);
+  }
+  if (lane == 0) red[wave] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    Acc a = red[0];
+    for (int w = 1; w < kThreads / 64; ++w) a = merge(a, red[w]);
+    p.token[r] = a.i;
+    if (p.prob) p.prob[r] = __builtin_amdgcn_exp2f((a.z - a.m) * kLog2e) / a.s;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_token_sample(const SampleArgs& a, hipStream_t stream) {
+  SampleParams p;
+  p.logits = (const char*)a.logits;
+  p.token = a.token;
+  p.prob = a.prob;
+  p.row_stride_bytes = a.row_stride * (a.bf16 ? 2 : 4);
+  p.V = a.V;
+  p.bf16 = a.bf16;
+  p.inv_t = 1.0f / a.temperature;
+  p.k0 = (uint32_t)(a.seed & 0xffffffffu);
+  p.k1 = (uint32_t)(a.seed >> 32);
+  p.step = a.step;
+  hipLaunchKernelGGL(cover_token_sample_kernel, dim3((unsigned)a.R), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cover

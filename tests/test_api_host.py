@@ -228,3 +228,20 @@ def test_attn_rect_needs_a_workspace():
     assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=None) == cover.COVER_ERR_INVALID
     assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=FAKE + 4) == cover.COVER_ERR_INVALID
     assert cover.rect_workspace(1, 32, 256, 4) == 32 * 4 * 256 * cover.COVER_RECT_RECORD
+
+
+def test_token_sample_rejects_bad_arguments():
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    lib = cover.lib()
+    good = cover.TokenDesc(4, 1000, cover.COVER_BF16, 1008)
+    call = lambda d, T=1.0, logits=FAKE, tok=FAKE: lib.cover_token_sample(
+        p(logits), T, 1, 0, p(tok), None, None if d is None else ctypes.byref(d), None)
+    assert call(None) == cover.COVER_ERR_INVALID
+    assert call(good, T=0.0) == cover.COVER_ERR_INVALID
+    assert call(good, T=-1.0) == cover.COVER_ERR_INVALID
+    assert call(good, T=float("inf")) == cover.COVER_ERR_INVALID
+    assert call(good, T=float("nan")) == cover.COVER_ERR_INVALID
+    assert call(good, tok=None) == cover.COVER_ERR_INVALID
+    assert call(good, logits=FAKE + 8) == cover.COVER_ERR_INVALID
+    assert call(cover.TokenDesc(4, 1000, cover.COVER_BF16, 1004)) == cover.COVER_ERR_INVALID
+    assert call(cover.TokenDesc(0, 1000, cover.COVER_BF16, 1008), logits=None, tok=None) == cover.COVER_OK
