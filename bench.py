@@ -73,7 +73,8 @@ def main() -> int:
     ap.add_argument("--only", choices=["attn", "select"], default=None)
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--kernel", choices=["token_stats", "attn_stats"], default=None)
+    ap.add_argument("--kernel", choices=["token_stats", "token_sample", "attn_stats",
+                                         "decode_update"], default=None)
     ap.add_argument("--lm-scale", type=float, default=8.0,
                     help="loop workload: LM-head weights scaled by this (peaked distributions)")
     ap.add_argument("--max-steps", type=int, default=2048, help="loop workload: step budget")
@@ -281,6 +282,42 @@ def bench_producer(args, dev, stream) -> int:
         nbytes = R * V * 2 + R * 16  # logits once; token id in; logp, conf, argmax out
         cfg = {"workload": f"LLaDA-8B LM-head block: R={R} positions x V={V} bf16 logits"}
         bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+    elif args.kernel == "token_sample":
+        R, V = 256, 126464
+        t = synth.token_inputs(R, V, seed=args.seed)
+        logits = t["buffer"].to(dev)[:, :V]
+        tok = torch.empty(R, device=dev, dtype=torch.int32)
+        prob = torch.empty(R, device=dev, dtype=torch.float32)
+        desc = cover.TokenDesc(R, V, cover.COVER_BF16, logits.stride(0))
+        cargs = [cover._ptr(logits), ctypes.c_float(0.3), ctypes.c_uint64(args.seed),
+                 ctypes.c_uint32(1), cover._ptr(tok), cover._ptr(prob), ctypes.byref(desc),
+                 cover._stream(stream)]
+        fn = cover.lib().cover_token_sample
+        run = lambda: fn(*cargs)
+        nbytes = R * V * 2 + R * 8  # logits once; token and probability out
+        cfg = {"workload": f"LLaDA-8B LM-head block: R={R} positions x V={V} bf16 logits, T=0.3"}
+        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+    elif args.kernel == "decode_update":
+        B, Lr = 1, 256
+        u = synth.update_inputs(B, Lr, seed=args.seed)
+        t = {k: u[k].to(dev) for k in ("tokens", "argmax", "conf", "seed_idx", "n_seed",
+                                         "remask_count")}
+        outs = [torch.empty((B, Lr), device=dev, dtype=torch.uint8) for _ in range(2)] + \
+               [torch.empty((B, 5), device=dev, dtype=torch.int32)]
+        last = torch.full((B, Lr), -1, device=dev, dtype=torch.int32)
+        ff = torch.empty(B, device=dev, dtype=torch.int32)
+        desc = cover.UpdateDesc(B, Lr, t["seed_idx"].shape[1], u["pos_offset"], u["mask_id"], 15,
+                                5, 0.9, 0)
+        # the state changes in place each launch; the work per launch stays the same shape
+        cargs = [cover._ptr(t[k]) for k in ("tokens", "argmax", "conf", "seed_idx", "n_seed",
+                                            "remask_count")] + [cover._ptr(o) for o in outs] + \
+                [cover._ptr(last), cover._ptr(ff), ctypes.byref(desc), cover._stream(stream)]
+        fn = cover.lib().cover_decode_update
+        run = lambda: fn(*cargs)
+        nbytes = None
+        flops = 0
+        cfg = {"workload": f"LLaDA-8B generated block: B={B} Lr={Lr}, 16 seeds, cap 15"}
+        bound, unit, peak = "latency", "us", None
     else:
         a = synth.stats_inputs("llada", seed=args.seed)
         t = {k: a[k].to(dev) for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx",
@@ -317,11 +354,14 @@ def bench_producer(args, dev, stream) -> int:
     us = e0.elapsed_time(e1) * 1e3 / args.steps
     if nbytes is not None:
         achieved = nbytes / (us * 1e-6) / 1e9
-    else:
+    elif peak is not None:
         achieved = flops / (us * 1e-6) / 1e12
+    else:  # latency-bound with no meaningful rate: the launch time itself
+        achieved = us
     print(json.dumps({"kernel": args.kernel, "us_per_launch": round(us, 3), "steps": args.steps,
                       "config": cfg, "roofline": {"bound": bound, "achieved": round(achieved, 2),
-                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
+                      "peak": peak, "unit": unit,
+                      "frac": round(achieved / peak, 4) if peak else None,
                       "algorithmic_bytes_per_launch": nbytes}}))
     return 0
 
