@@ -355,8 +355,8 @@ cover_status cover_decode_update(int32_t* tokens, const int32_t* argmax, const f
  * cover_debug_status -- the contract checks enabled by COVER_DEBUG=1 (a debugging aid for
  * integrations; not for production paths).
  *
- * While the environment variable COVER_DEBUG is "1", every cover_attn_fwd and
- * cover_attn_stats call first checks its seed lists, and every cover_select_seeds call its
+ * While the environment variable COVER_DEBUG is "1", every cover_attn_fwd, cover_attn_rect
+ * and cover_attn_stats call first checks its seed lists, and every cover_select_seeds call its
  * inputs on U_t, with a small kernel on the same stream; a violation sets bits of a status
  * word kept on the current GPU:
  */

@@ -1,0 +1,31 @@
+"""Host-side checks of bench.py (no GPU): the multi-GPU request is refused with a message,
+and the HBM traffic figure is taken from the committed profile only while the kernel source
+it was measured on is unchanged."""
+import os
+import re
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "single GPU" in r.stderr
+
+
+def test_traffic_figure_tracks_the_kernel_source():
+    text = open(bench.TRAFFIC_SUMMARY).read()
+    m = re.search(r"^traffic_bytes_per_launch:\s*(\d+)\s+workload:\s*(\w+)\s+source:\s*(\w+)",
+                  text, flags=re.M)
+    assert m, "the profile must carry its machine-readable line"
+    got = bench.measured_traffic(m.group(2))
+    if m.group(3) == bench.kernel_source_hash():
+        assert got == int(m.group(1))
+    else:
+        assert got is None
+    assert bench.measured_traffic("no-such-workload") is None

@@ -115,3 +115,15 @@ def test_attention_masses_check_their_seed_lists(debug):
                            dev["masked"], dev["drafted"], a["r0"])
     torch.cuda.synchronize()
     assert cover.debug_status(clear=True) == cover.COVER_DEBUG_SEED_DUPLICATE
+
+
+def test_block_attention_checks_its_seed_list(debug):
+    announce("debug rect seeds")
+    a = synth.attn_inputs("llada", seed=4)
+    q, kl, vl, kc, vc = (a[k].cuda() for k in ("q", "k_live", "v_live", "k_cache", "v_cache"))
+    si = a["seed_idx"].clone()
+    si[0, 1] = si[0, 0]  # a duplicate
+    qb = q[:, :, 768:].contiguous()
+    cover.cover_attn_rect(qb, kl, vl, kc, vc, 768, si.cuda(), a["n_seed"].cuda())
+    torch.cuda.synchronize()
+    assert cover.debug_status(clear=True) == cover.COVER_DEBUG_SEED_DUPLICATE
