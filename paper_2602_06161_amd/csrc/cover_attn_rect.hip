@@ -72,6 +72,17 @@ __device__ __forceinline__ uint32_t k_off(int row, int c) { return row * kRow + 
 __device__ __forceinline__ uint32_t v_chunk(int row, int c) { return row * kRow + ((c ^ ((row & 3) << 2)) << 4); }
 __device__ __forceinline__ uint32_t v_elem(int row, int col) { return v_chunk(row, col >> 3) + ((col & 7) << 1); }
 
+// max / sum of x over a query row's lane pair (lanes l and l ^ 32), on the VALU: the swap
+// leaves one copy of each lane's own value and one of its partner's in the two results
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
 }
@@ -199,7 +210,7 @@ __global__ __launch_bounds__(kThreads, 2) void cover_attn_rect_kernel(const Rect
         s[r] = t;
         mx = __builtin_fmaxf(mx, t);
       }
-      mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32));
+      mx = pair_max(mx);
       const float mn = __builtin_fmaxf(m, mx);
       if (__builtin_amdgcn_ballot_w64(mn > m)) {  // some row's max grew: rescale
         const float alpha = __builtin_amdgcn_exp2f(m - mn);
@@ -244,7 +255,7 @@ __global__ __launch_bounds__(kThreads, 2) void cover_attn_rect_kernel(const Rect
 #pragma unroll
       for (int e = 0; e < 8; ++e) dot = __builtin_fmaf((float)qreg[ks][e], (float)kv8[e], dot);
     }
-    dot += __shfl_xor(dot, 32);
+    dot = pair_sum(dot);
     const float t = dot * p.c2;
     const float mn = __builtin_fmaxf(m, t);
     const float alpha = __builtin_amdgcn_exp2f(m - mn);
@@ -261,7 +272,7 @@ __global__ __launch_bounds__(kThreads, 2) void cover_attn_rect_kernel(const Rect
         for (int e = 0; e < 4; ++e) o[db][4 * g + e] = __builtin_fmaf(pd, (float)vp[dim + e], o[db][4 * g + e] * alpha);
       }
   }
-  const float lt = l + __shfl_xor(l, 32);
+  const float lt = pair_sum(l);
   if (qrow0 + l32 >= p.Lq) return;
   float* rec = p.ws + (((int64_t)bh * p.n_split + split) * p.Lq + qrow0 + l32) * COVER_RECT_RECORD;
   const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
