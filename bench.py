@@ -93,8 +93,8 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build measures a single GPU only; the multi-GPU sharding of the "
-              "path is described in DESIGN.md but not built. Run with --gpus 1.", file=sys.stderr)
+        print("bench.py: measures a single GPU only (the path is not sharded across GPUs). "
+              "Run with --gpus 1.", file=sys.stderr)
         return 2
 
     import torch
