@@ -62,7 +62,11 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+// PER: positions per thread the register arrays hold (p.per <= PER).  With PER <= 4 the
+// argmax and the counters are requested together with the tokens (one round trip fewer).
+template <int PER>
 __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdParams p) {
+  constexpr bool kEarly = PER <= 4;
   __shared__ uint32_t seedbits[COVER_MAX_LR / 32];
   __shared__ uint32_t hist[256];
   // candidates, |D|, kept, replaced, remasked, masked after, flip-flops, forced candidates
@@ -77,16 +81,20 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   __syncthreads();
 
   // 1. per-position inputs, and the seed bitmap
-  int tok[kMaxPer];
-  float cf[kMaxPer];
+  int tok[PER], am[kEarly ? PER : 1], rc[kEarly ? PER : 1];
+  float cf[PER];
 #pragma unroll
-  for (int m = 0; m < kMaxPer; ++m) {
+  for (int m = 0; m < PER; ++m) {
     const int j = tid + m * nth;
     tok[m] = 0;
     cf[m] = 0.0f;
     if (m < p.per && j < p.Lr) {
       tok[m] = p.tokens[base + j];
       cf[m] = p.conf[base + j];
+      if constexpr (kEarly) {
+        am[m] = p.argmax[base + j];
+        rc[m] = p.remask_count[base + j];
+      }
     }
   }
   int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
@@ -97,10 +105,10 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   }
 
   // 2. candidate keys
-  uint64_t key[kMaxPer];
+  uint64_t key[PER];
   uint32_t cand = 0;
 #pragma unroll
-  for (int m = 0; m < kMaxPer; ++m) {
+  for (int m = 0; m < PER; ++m) {
     const int j = tid + m * nth;
     key[m] = 0;
     if (m < p.per && j < p.Lr && tok[m] == p.mask_id && cf[m] > p.tau) {
@@ -116,7 +124,7 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   if (total < p.min_draft) {  // too few above tau: the min_draft most confident masked ones
     cand = 0;
 #pragma unroll
-    for (int m = 0; m < kMaxPer; ++m) {
+    for (int m = 0; m < PER; ++m) {
       const int j = tid + m * nth;
       key[m] = 0;
       if (m < p.per && j < p.Lr && tok[m] == p.mask_id && cf[m] == cf[m]) {
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
       const uint64_t hi = shift == 56 ? 0ull : (~0ull << (shift + 8));
       const uint64_t pre = s_prefix;
 #pragma unroll
-      for (int m = 0; m < kMaxPer; ++m)
+      for (int m = 0; m < PER; ++m)
         if (((cand >> m) & 1u) && (key[m] & hi) == pre)
           atomicAdd(&hist[(uint32_t)(key[m] >> shift) & 255u], 1u);
       __syncthreads();
@@ -189,7 +197,7 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
   // 4. per-position update
   int n_d = 0, n_keep = 0, n_rep = 0, n_rm = 0, n_masked = 0, n_ff = 0;
 #pragma unroll
-  for (int m = 0; m < kMaxPer; ++m) {
+  for (int m = 0; m < PER; ++m) {
     const int j = tid + m * nth;
     if (m < p.per && j < p.Lr) {
       const int64_t e = base + j;
@@ -197,9 +205,13 @@ __global__ __launch_bounds__(kMaxThreads) void cover_update_kernel(const UpdPara
       // a listed seed at a masked position is no seed
       const bool seed = ((seedbits[j >> 5] >> (j & 31)) & 1u) && tok[m] != p.mask_id;
       int t = tok[m];
-      int cnt = p.remask_count[e];
+      int cnt;
+      if constexpr (kEarly) cnt = rc[m];
+      else cnt = p.remask_count[e];
       if (dr || seed) {
-        const int a = p.argmax[e];
+        int a;
+        if constexpr (kEarly) a = am[m];
+        else a = p.argmax[e];
         if (dr) {
           t = a;
           ++n_d;
@@ -254,7 +266,12 @@ hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream) {
   if (nth > kMaxThreads) nth = kMaxThreads;
   p.per = (a.Lr + nth - 1) / nth;
   if (p.per > kMaxPer) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(cover_update_kernel, dim3((unsigned)a.B), dim3((unsigned)nth), 0, stream, p);
+  if (p.per <= 1)
+    hipLaunchKernelGGL(cover_update_kernel<1>, dim3((unsigned)a.B), dim3((unsigned)nth), 0, stream, p);
+  else if (p.per <= 4)
+    hipLaunchKernelGGL(cover_update_kernel<4>, dim3((unsigned)a.B), dim3((unsigned)nth), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cover_update_kernel<kMaxPer>, dim3((unsigned)a.B), dim3((unsigned)nth), 0, stream, p);
   return hipGetLastError();
 }
 
