@@ -220,8 +220,9 @@ typedef struct {
 
 /* Largest response region cover_attn_stats accepts. */
 #define COVER_STATS_MAX_LR 2048
-/* Workspace of cover_attn_stats in floats: B * Hq * 2 * Lr. */
-#define COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr) ((int64_t)(B) * (Hq) * 2 * (Lr))
+/* Workspace of cover_attn_stats in floats: B * Hq * (1 + ceil(Lr / 32)) * Lr. */
+#define COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr) \
+  ((int64_t)(B) * (Hq) * (1 + ((int64_t)(Lr) + 31) / 32) * (Lr))
 
 /*
  * cover_attn_stats -- the in/out attention masses of Sec. 5.3 from the last layer's

@@ -70,7 +70,7 @@ class StatsDesc(ctypes.Structure):
 
 def attn_stats_workspace(B: int, Hq: int, Lr: int) -> int:
     """Floats of workspace cover_attn_stats needs (COVER_ATTN_STATS_WORKSPACE)."""
-    return B * Hq * 2 * Lr
+    return B * Hq * (1 + (Lr + 31) // 32) * Lr
 
 
 _lib = None

@@ -11,11 +11,13 @@
 // w_qj = exp(scale q.K^(q)_j - lse_q) (the same leave-one-out rows the attention computes,
 // normalised over the whole sequence by the forward pass's lse), averaged over query heads:
 //   d_in(j)  = (1/Hq) sum_h sum_{q masked} w_qj,    d_out(j) = (1/Hq) sum_h sum_{i drafted} w_ji
-// One workgroup per (batch row, query head); each of its waves takes 32-query blocks of the
-// region and forms both S = Q K^T and S^T = K Q^T tile by tile (the same operand registers,
-// swapped), so each mass is a sum inside a lane.  Per-head masses go to a caller-provided
-// workspace and a second kernel averages them over heads; every sum runs in a fixed order,
-// so the results do not depend on scheduling.
+// One workgroup per (batch row, query head, group of 32-key tiles), about 256 in all; each of
+// its waves takes 32-query blocks of the region and forms both S = Q K^T and S^T = K Q^T over
+// the group's key tiles (the same operand registers, swapped), so each mass is a sum inside a
+// lane.  A key's d_in is complete inside its group's workgroup; d_out gets one partial per
+// key group.  Both go to a caller-provided workspace and a second kernel adds the partials
+// and averages over heads; every sum runs in a fixed order, so the results do not depend on
+// scheduling.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -172,10 +174,11 @@ struct StatParams {
   const float* lse;
   const uint8_t* masked;
   const uint8_t* drafted;
-  float* ws;  // [B, Hq, 2, Lr]: per head, d_in and d_out before the average over heads
+  float* ws;  // [B, Hq, 1 + KG, Lr]: per head, d_in, then the KG partials of d_out
   float* d_in;
   float* d_out;
   int B, Hq, Hkv, L, d, max_seeds, group, r0, Lr, NB;
+  int KG, TPG;  // key groups, 32-key tiles per group
   float scale;
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
@@ -193,7 +196,10 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
   __shared__ float sdin[kStatWaves][COVER_STATS_MAX_LR];  // per-wave d_in partials over its blocks
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hl = lane >> 5, l32 = lane & 31;
-  const int h = blockIdx.x % p.Hq, b = blockIdx.x / p.Hq;
+  const int kg = blockIdx.x % p.KG, bh = blockIdx.x / p.KG;
+  const int h = bh % p.Hq, b = bh / p.Hq;
+  const int kt0 = kg * p.TPG, kt1 = min(p.NB, kt0 + p.TPG);  // this workgroup's key tiles
+  float* const wsh = p.ws + ((int64_t)b * p.Hq + h) * (1 + p.KG) * p.Lr;
   const int g = h / p.group;
   const int L = p.L;
   // seed bitmap of this sequence; the d_in rows start at zero
@@ -253,9 +259,9 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
     for (int r = 0; r < 16; ++r) lse_r[r] = lrow[p.r0 + rb + min(8 * (r >> 2) + 4 * hl + (r & 3), qn - 1)];
     float dout = 0.0f;  // this lane's query: sum over drafted keys (its 16 of each tile)
     bf16x8 kf[KS], kn_f[KS];
-    load_k(kf, 0);
-    for (int kt = 0; kt < p.NB; ++kt) {
-      if (kt + 1 < p.NB) load_k(kn_f, kt + 1);  // the next tile's rows are requested first
+    if (kt0 < kt1) load_k(kf, kt0);
+    for (int kt = kt0; kt < kt1; ++kt) {
+      if (kt + 1 < kt1) load_k(kn_f, kt + 1);  // the next tile's rows are requested first
       const int kb = kt * 32;
       const int kn = min(32, p.Lr - kb);
       f32x16 st = {}, sq = {};  // S^T (lane = query, registers = keys), S (lane = key)
@@ -284,33 +290,53 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
       for (int ks = 0; ks < KS; ++ks) kf[ks] = kn_f[ks];
     }
     dout += __shfl_xor(dout, 32);
-    if (hl == 0 && l32 < qn) p.ws[(((int64_t)b * p.Hq + h) * 2 + 1) * p.Lr + rb + l32] = dout;
+    if (hl == 0 && l32 < qn) wsh[(int64_t)(1 + kg) * p.Lr + rb + l32] = dout;
   }
   __syncthreads();
-  // d_in of this head: the waves' rows added in a fixed order
-  for (int j = tid; j < p.Lr; j += 64 * kStatWaves) {
+  // d_in of this head at the group's keys: the waves' rows added in a fixed order
+  const int j1 = min(p.Lr, kt1 * 32);
+  for (int j = kt0 * 32 + tid; j < j1; j += 64 * kStatWaves) {
     float s = 0.0f;
 #pragma unroll
     for (int w = 0; w < kStatWaves; ++w) s += sdin[w][j];
-    p.ws[(((int64_t)b * p.Hq + h) * 2 + 0) * p.Lr + j] = s;
+    wsh[j] = s;
   }
 }
 
-// d_in(j) = (1/Hq) sum_h ws_in[h][j], d_out(j) = (1/Hq) sum_h ws_out[h][j], heads in order
+// d_in(j) = (1/Hq) sum_h ws[h][0][j], d_out(j) = (1/Hq) sum_h sum_g ws[h][1+g][j].  A block
+// of 32 keys x 8 head lanes: lane y adds heads y, y+8, ... (groups in order inside each
+// head), then the 8 lane sums are added in order: a fixed order, so deterministic.
 __global__ __launch_bounds__(256) void cover_attn_stats_reduce_kernel(const StatParams p) {
-  const int b = blockIdx.y;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= p.Lr) return;
-  const float* w = p.ws + (int64_t)b * p.Hq * 2 * p.Lr + j;
+  __shared__ float sin_[8][32], sout[8][32];
+  const int b = blockIdx.y, jx = threadIdx.x & 31, hy = threadIdx.x >> 5;
+  const int j = blockIdx.x * 32 + jx;
+  const int rec = 1 + p.KG;
   float din = 0.0f, dout = 0.0f;
+  if (j < p.Lr) {
+    const float* w = p.ws + (int64_t)b * p.Hq * rec * p.Lr + j;
+    for (int h = hy; h < p.Hq; h += 8) {
+      const float* wh = w + (int64_t)(rec * h) * p.Lr;
+      din += wh[0];
+      float part = 0.0f;
 #pragma unroll 8
-  for (int h = 0; h < p.Hq; ++h) {
-    din += w[(int64_t)(2 * h) * p.Lr];
-    dout += w[(int64_t)(2 * h + 1) * p.Lr];
+      for (int g = 0; g < p.KG; ++g) part += wh[(int64_t)(1 + g) * p.Lr];
+      dout += part;
+    }
   }
-  const float inv = 1.0f / (float)p.Hq;
-  p.d_in[(int64_t)b * p.Lr + j] = din * inv;
-  p.d_out[(int64_t)b * p.Lr + j] = dout * inv;
+  sin_[hy][jx] = din;
+  sout[hy][jx] = dout;
+  __syncthreads();
+  if (hy == 0 && j < p.Lr) {
+    float a = 0.0f, c = 0.0f;
+#pragma unroll
+    for (int y = 0; y < 8; ++y) {
+      a += sin_[y][jx];
+      c += sout[y][jx];
+    }
+    const float inv = 1.0f / (float)p.Hq;
+    p.d_in[(int64_t)b * p.Lr + j] = a * inv;
+    p.d_out[(int64_t)b * p.Lr + j] = c * inv;
+  }
 }
 
 }  // namespace
@@ -346,10 +372,18 @@ hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream) {
   p.group = a.Hq / a.Hkv;
   p.r0 = a.r0; p.Lr = a.Lr;
   p.NB = (a.Lr + 31) / 32;
+  // key groups: about 256 workgroups in all (at most one group per tile)
+  {
+    const int64_t heads = (int64_t)a.B * a.Hq;
+    int kg = (int)((256 + heads - 1) / heads);
+    kg = kg < 1 ? 1 : (kg > p.NB ? p.NB : kg);
+    p.TPG = (p.NB + kg - 1) / kg;
+    p.KG = (p.NB + p.TPG - 1) / p.TPG;  // no empty group
+  }
   p.scale = a.scale;
   p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
   p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
-  const int64_t nwg = (int64_t)a.B * a.Hq;
+  const int64_t nwg = (int64_t)a.B * a.Hq * p.KG;
   if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
   if (a.d == 128)
     hipLaunchKernelGGL(cover_attn_stats_kernel<128>, dim3((unsigned)nwg), dim3(64 * kStatWaves), 0, stream, p);
@@ -357,7 +391,7 @@ hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(cover_attn_stats_kernel<64>, dim3((unsigned)nwg), dim3(64 * kStatWaves), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(cover_attn_stats_reduce_kernel, dim3((unsigned)((a.Lr + 255) / 256), (unsigned)a.B),
+  hipLaunchKernelGGL(cover_attn_stats_reduce_kernel, dim3((unsigned)((a.Lr + 31) / 32), (unsigned)a.B),
                      dim3(256), 0, stream, p);
   return hipGetLastError();
 }

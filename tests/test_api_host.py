@@ -169,7 +169,7 @@ def test_attn_stats_rejects_missing_buffers():
     assert _stats(None) == cover.COVER_ERR_INVALID
     assert _stats(good, ws=None) == cover.COVER_ERR_INVALID
     assert _stats(good, lse=None) == cover.COVER_ERR_INVALID
-    assert cover.attn_stats_workspace(1, 32, 256) == 32 * 2 * 256
+    assert cover.attn_stats_workspace(1, 32, 256) == 32 * 9 * 256
 
 
 def _upd(desc, tok=FAKE, si=FAKE, ns=FAKE, counts=None, last=None, ff=None):
