@@ -2,8 +2,13 @@
 drawn tokens follow softmax(x / T) (chi-square over 20000 rows of the same logits, several
 temperatures), a vanishing temperature gives the argmax, the uniforms are uniform on (0, 1)
 and exact in fp32, draws depend on every counter component, and planted mistakes (x * T for
-x / T, noise dropped, noise sign flipped, a counter component ignored) are caught."""
+x / T, noise dropped, noise sign flipped, a counter component ignored) are caught.  The
+generator itself is pinned by the three published Random123 known-answer vectors
+(tests/golden/philox4x32_10_kat.json), which one-line mistakes in its multipliers, key
+schedule, round count or output order all fail."""
 import inspect
+import json
+import os
 
 import numpy as np
 import pytest
@@ -97,3 +102,41 @@ def test_planted_generator_mistakes_are_caught(old, new):
         assert not np.array_equal(su(2, 16, 123, 5), oracle.sample_uniforms(2, 16, 123, 5))
         return
     assert not _uniform_ok(_mutant(oracle.sample_uniforms, old, new))
+
+
+# ---- known answers of the generator itself ----------------------------------------------
+_KAT = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.json")))
+
+
+def _kat_ok(fn):
+    for v in _KAT["vectors"]:
+        c = [int(x, 16) for x in v["counter"]]
+        k = [int(x, 16) for x in v["key"]]
+        got = [int(w) for w in fn(*c, *k)]
+        if got != [int(x, 16) for x in v["out"]]:
+            return False
+    return True
+
+
+def test_philox_known_answers():
+    # the published Random123 vectors pin the multipliers, the Weyl key schedule, the round
+    # count and the output word order
+    assert _kat_ok(oracle.philox4x32_10)
+
+
+@pytest.mark.parametrize("old,new", [
+    ("_PHILOX_M[0]) * c[0]", "_PHILOX_M[1]) * c[0]"),                     # multipliers swapped
+    ("p1 = np.uint64(_PHILOX_M[1])", "p1 = np.uint64(_PHILOX_M[0])"),
+    ("c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]",
+     "c = [hi0 ^ c[1] ^ k0, lo0, hi1 ^ c[3] ^ k1, lo1]"),                  # products exchanged
+    ("return c", "return [c[1], c[0], c[2], c[3]]"),                      # output words swapped
+    ("return c", "return c[::-1]"),                                       # output order reversed
+    ("        if r:\n", "        if r > 1:\n"),                           # a key bump missing
+    ("k0 = (k0 + np.uint64(_PHILOX_W[0])) & _U32", "k0 = k0"),           # k0 never advanced
+    ("k1 = (k1 + np.uint64(_PHILOX_W[1])) & _U32",
+     "k1 = (k1 + np.uint64(_PHILOX_W[0])) & _U32"),                       # wrong Weyl constant
+    ("for r in range(10):", "for r in range(9):"),                        # a round missing
+    ("hi1 ^ c[1] ^ k0", "hi1 ^ c[1] ^ k1"),                               # keys exchanged
+])
+def test_planted_philox_mistakes_fail_the_known_answers(old, new):
+    assert not _kat_ok(_mutant(oracle.philox4x32_10, old, new))
