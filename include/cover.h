@@ -220,7 +220,8 @@ typedef struct {
 
 /* Largest response region cover_attn_stats accepts. */
 #define COVER_STATS_MAX_LR 2048
-/* Workspace of cover_attn_stats in floats: B * Hq * (1 + ceil(Lr / 32)) * Lr. */
+/* An upper bound of the workspace of cover_attn_stats in floats, valid for every launch:
+ * B * Hq * (1 + ceil(Lr / 32)) * Lr.  cover_attn_stats_workspace gives the exact need. */
 #define COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr) \
   ((int64_t)(B) * (Hq) * (1 + ((int64_t)(Lr) + 31) / 32) * (Lr))
 
@@ -237,8 +238,9 @@ typedef struct {
  * Arguments: q, k_live, k_cache, seed_idx, n_seed as for cover_attn_fwd (v is not needed);
  * lse fp32 [B,Hq,L] contiguous, as returned by cover_attn_fwd for the same inputs;
  * masked, drafted uint8 [B,Lr] (nonzero = member; device); d_in, d_out fp32 [B,Lr]
- * (device outputs); workspace: device fp32 buffer of COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr)
- * floats owned by the caller (its contents on entry are ignored, on exit unspecified).
+ * (device outputs); workspace: device fp32 buffer of at least
+ * cover_attn_stats_workspace(B, Hq, Lr) floats (COVER_ATTN_STATS_WORKSPACE(B, Hq, Lr) always
+ * suffices) owned by the caller (its contents on entry are ignored, on exit unspecified).
  * Two kernel launches on `stream`; partial sums are added in a fixed order, so the results
  * are deterministic.  Weights are formed in fp32 from the fp32 lse.
  * Returns COVER_ERR_UNSUPPORTED for a dtype other than bf16, d not in {64, 128},
@@ -249,6 +251,14 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
                               const uint8_t* masked, const uint8_t* drafted,
                               float* d_in, float* d_out, float* workspace,
                               const cover_stats_desc* desc, hipStream_t stream);
+
+/*
+ * cover_attn_stats_workspace -- floats of workspace a cover_attn_stats call with these B, Hq
+ * and Lr uses: B * Hq * (1 + G) * Lr, with G the number of key groups the launch splits the
+ * region's 32-key tiles into (about 256 workgroups in all; G <= ceil(Lr / 32)).  A host
+ * function: no GPU work.  Returns -1 for negative arguments.
+ */
+int64_t cover_attn_stats_workspace(int32_t B, int32_t Hq, int32_t Lr);
 
 /*
  * Block-query attention description: the attention problem of cover_attn_fwd (same fields

@@ -20,7 +20,8 @@ COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
 COVER_RECT_RECORD = 68
 
-EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_debug_status", "cover_decode_update",
+EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_attn_stats_workspace",
+            "cover_debug_status", "cover_decode_update",
             "cover_select_seeds", "cover_status_str", "cover_token_sample", "cover_token_stats",
             "cover_version")
 # status bits of the contract checks that COVER_DEBUG=1 enables (cover_debug_status)
@@ -69,8 +70,12 @@ class StatsDesc(ctypes.Structure):
 
 
 def attn_stats_workspace(B: int, Hq: int, Lr: int) -> int:
-    """Floats of workspace cover_attn_stats needs (COVER_ATTN_STATS_WORKSPACE)."""
-    return B * Hq * (1 + (Lr + 31) // 32) * Lr
+    """Floats of workspace a cover_attn_stats call of this size uses (the library's
+    cover_attn_stats_workspace)."""
+    n = lib().cover_attn_stats_workspace(int(B), int(Hq), int(Lr))
+    if n < 0:
+        raise ValueError("negative size")
+    return int(n)
 
 
 _lib = None
@@ -101,6 +106,8 @@ def lib():
         L.cover_token_sample.restype = ctypes.c_int
         L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
         L.cover_attn_stats.restype = ctypes.c_int
+        L.cover_attn_stats_workspace.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+        L.cover_attn_stats_workspace.restype = ctypes.c_int64
         L.cover_status_str.argtypes = [ctypes.c_int]
         L.cover_status_str.restype = ctypes.c_char_p
         L.cover_version.argtypes = []
@@ -374,9 +381,13 @@ def cover_attn_stats(q, k_live, k_cache, seed_idx, n_seed, lse, masked, drafted,
     dev = q.device
     d_in = torch.empty((B, Lr), device=dev, dtype=torch.float32)
     d_out = torch.empty((B, Lr), device=dev, dtype=torch.float32)
+    need = attn_stats_workspace(B, Hq, Lr)
     if workspace is None:
-        workspace = torch.empty(max(1, attn_stats_workspace(B, Hq, Lr)), device=dev,
-                                dtype=torch.float32)
+        workspace = torch.empty(max(1, need), device=dev, dtype=torch.float32)
+    elif (workspace.dtype != torch.float32 or not workspace.is_contiguous()
+          or workspace.numel() < need or workspace.device != dev):
+        raise ValueError(f"workspace must be a contiguous fp32 tensor of at least {need} floats "
+                         f"on {dev}")
     desc = StatsDesc(attn_desc(q, k_live, max_seeds, scale), int(r0), int(Lr))
     st = lib().cover_attn_stats(_ptr(q), _ptr(k_live), _ptr(k_cache), _ptr(seed_idx),
                                 _ptr(n_seed), _ptr(lse), _ptr(masked), _ptr(drafted), _ptr(d_in),

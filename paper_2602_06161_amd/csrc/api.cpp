@@ -154,6 +154,12 @@ cover_status cover_token_sample(const void* logits, float temperature, uint64_t 
   return hip_status(cover::launch_token_sample(a, stream));
 }
 
+int64_t cover_attn_stats_workspace(int32_t B, int32_t Hq, int32_t Lr) {
+  if (B < 0 || Hq < 0 || Lr < 0) return -1;
+  if (B == 0 || Hq == 0 || Lr == 0) return 0;
+  return cover::stats_workspace_floats(B, Hq, Lr);
+}
+
 cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
                               const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
                               const uint8_t* masked, const uint8_t* drafted,

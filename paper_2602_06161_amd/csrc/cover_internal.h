@@ -112,6 +112,10 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream);
 hipError_t launch_token_sample(const SampleArgs& a, hipStream_t stream);
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
+// key groups of the attention-mass launch (32-key tiles per group, groups) and the workspace
+// floats that launch uses
+void stats_key_groups(int B, int Hq, int Lr, int* tpg, int* kg);
+int64_t stats_workspace_floats(int B, int Hq, int Lr);
 hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream);
 hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream);  // bf16, d = 128
 

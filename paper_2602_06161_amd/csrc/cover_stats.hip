@@ -355,6 +355,23 @@ hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+void stats_key_groups(int B, int Hq, int Lr, int* tpg, int* kg_out) {
+  // key groups: about 256 workgroups in all (at most one group per 32-key tile, none empty)
+  const int nb = (Lr + 31) / 32;
+  const int64_t heads = (int64_t)B * Hq;
+  int64_t kg = heads > 0 ? (256 + heads - 1) / heads : 1;
+  kg = kg < 1 ? 1 : (kg > nb ? nb : kg);
+  const int t = kg > 0 ? (int)((nb + kg - 1) / kg) : 1;
+  *tpg = t;
+  *kg_out = t > 0 ? (nb + t - 1) / t : 0;
+}
+
+int64_t stats_workspace_floats(int B, int Hq, int Lr) {
+  int tpg, kg;
+  stats_key_groups(B, Hq, Lr, &tpg, &kg);
+  return (int64_t)B * Hq * (1 + kg) * Lr;
+}
+
 hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream) {
   StatParams p;
   p.q = (const __bf16*)a.q;
@@ -372,14 +389,7 @@ hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream) {
   p.group = a.Hq / a.Hkv;
   p.r0 = a.r0; p.Lr = a.Lr;
   p.NB = (a.Lr + 31) / 32;
-  // key groups: about 256 workgroups in all (at most one group per tile)
-  {
-    const int64_t heads = (int64_t)a.B * a.Hq;
-    int kg = (int)((256 + heads - 1) / heads);
-    kg = kg < 1 ? 1 : (kg > p.NB ? p.NB : kg);
-    p.TPG = (p.NB + kg - 1) / kg;
-    p.KG = (p.NB + p.TPG - 1) / p.TPG;  // no empty group
-  }
+  stats_key_groups(a.B, a.Hq, a.Lr, &p.TPG, &p.KG);
   p.scale = a.scale;
   p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
   p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;

@@ -1,9 +1,11 @@
 """GPU parity of cover_attn_fwd (through the C ABI) against the fp64 oracle.
 
 Bar: fp32 max-abs 1e-5; bf16 |gpu - oracle| <= 2e-2 + 1e-2 |oracle| on out and 2e-2 on lse.
-Small shapes are compared on every row (several query/key tiles and a ragged tail); the
-full-size workloads are compared on every seed row of sampled heads plus random rows, in
-the same launch configuration the benchmark times.
+Small shapes are compared on every row (several query/key tiles and a ragged tail), so are
+sequences of more than 64 key stages with seeds in every stage window and seed lists longer
+than the on-chip list; the LLaDA-8B and Dream-7B layer shapes are compared on every row and
+the batched long-context shape on two whole batch rows, in the launch configuration the
+benchmark times.
 """
 import numpy as np
 import pytest
@@ -213,3 +215,88 @@ def test_full_size_config_sampled_rows(name, hpb):
     l = lse.reshape(-1)[torch.from_numpy(rows).cuda()]
     check_attn(o, l, ref, lref, torch.bfloat16, name)
     assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+
+
+def _explicit(seed, B, Hq, Hkv, L, d, per_row, max_seeds=None):
+    """Inputs with an explicit seed list per batch row (per_row[b]: positions, any order)."""
+    cfg = synth.AttnConfig("custom", B, Hq, Hkv, L, d, "bf16", 0, L, 0, "independent")
+    a = synth.attn_inputs(cfg, seed=seed, max_seeds=0)
+    ms = max_seeds if max_seeds is not None else max(len(p) for p in per_row)
+    si = np.full((B, ms), -1, np.int32)
+    ns = np.zeros((B,), np.int32)
+    for b, pos in enumerate(per_row):
+        pos = np.array(sorted(set(int(x) for x in pos)), np.int32)
+        assert pos.size <= ms and (pos.size == 0 or (pos[0] >= 0 and pos[-1] < L))
+        si[b, : pos.size] = pos
+        ns[b] = pos.size
+    a["seed_idx"], a["n_seed"] = torch.from_numpy(si), torch.from_numpy(ns)
+    return a
+
+
+def _stage_spanning_seeds(L, rng, extra=0):
+    """Seeds on the first and last rows of stages 0, 31, 32, 33, 63, 64, 65 (64 keys per stage;
+    those that exist below L), the last position, plus `extra` random positions."""
+    pos = {0, L - 1}
+    for s in (0, 1, 31, 32, 33, 63, 64, 65, 95, 96, 127, 128):
+        for r in (0, 17, 63):
+            if s * 64 + r < L:
+                pos.add(s * 64 + r)
+    if extra:
+        pos |= set(rng.choice(L, size=extra, replace=False).tolist())
+    return sorted(pos)
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("L", [4200, 8200])
+def test_long_sequence_every_row(L, d):
+    """More than 64 key stages (the per-stage seed windows are refreshed every 32 stages and
+    looked up past stage 64), a ragged last stage (4200 = 65 x 64 + 40; 8200 = 128 x 64 + 8),
+    seeds in stages 0..128 including the last position, and a second batch row with its own
+    seed set."""
+    rng = np.random.default_rng(L + d)
+    rows = [_stage_spanning_seeds(L, rng), rng.choice(L, size=40, replace=False)]
+    Hq = 2 if L < 8000 else 1
+    announce(f"bf16 long sequence B2 Hq{Hq} Hkv1 L{L} d{d}, {len(rows[0])}/40 seeds")
+    a = _explicit(20 + L, 2, Hq, 1, L, d, rows)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, f"long L{L} d{d}")
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_more_than_256_seeds(d):
+    """Seed lists longer than the 256 entries staged on chip (the rest is read from memory):
+    300 and 257 seeds in two batch rows, over more than 64 stages in the first."""
+    rng = np.random.default_rng(300 + d)
+    rows = [rng.choice(4200, size=300, replace=False), rng.choice(2000, size=257, replace=False)]
+    announce(f"bf16 B2 Hq4 Hkv2 L4200 d{d}, 300 / 257 seeds")
+    a = _explicit(31 + d, 2, 4, 2, 4200, d, rows, max_seeds=320)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, f"300 seeds d{d}")
+
+
+@pytest.mark.parametrize("name", ["llada", "dream"])
+def test_full_size_config_every_row(name):
+    """Every output row of the LLaDA-8B and Dream-7B layer shapes against the oracle, in the
+    launch configuration the benchmark times."""
+    announce(f"{name} full size, every row")
+    a = synth.attn_inputs(name, seed=0)
+    out, lse = _run(a)
+    ref, lref = _oracle(a)
+    check_attn(out, lse, ref, lref, torch.bfloat16, name)
+
+
+def test_batched_whole_batch_rows():
+    """Two whole batch rows (all 32 heads x 2048 positions each) of the batched long-context
+    shape, each batch row with its own 64 seeds."""
+    announce("batched B8 H32 L2048, batch rows 0 and 5 whole")
+    a = synth.attn_inputs("batched", seed=0)
+    out, lse = _run(a)
+    c = a["cfg"]
+    per = c.Hq * c.L
+    rows = np.concatenate([np.arange(b * per, (b + 1) * per, dtype=np.int64) for b in (0, 5)])
+    ref, lref = _oracle(a, rows=rows)
+    o = out.reshape(-1, c.d)[torch.from_numpy(rows).cuda()]
+    l = lse.reshape(-1)[torch.from_numpy(rows).cuda()]
+    check_attn(o, l, ref, lref, torch.bfloat16, "batched rows 0, 5")

@@ -120,6 +120,45 @@ def test_attn_stats_vs_oracle(d, r0, Lr):
     _stats_case(a, r0, masked, drafted)
 
 
+@pytest.mark.parametrize("B,Hq,Hkv,L,r0,Lr", [
+    (2, 4, 2, 1100, 0, 1100),    # 35 key tiles in 18 groups of 2, the last group one tile
+    (1, 32, 32, 2048, 0, 2048),  # 64 key tiles in 8 groups of 8
+    (1, 28, 4, 1500, 300, 1111),  # 35 tiles in 9 groups of 4, the last group three tiles (GQA)
+])
+def test_attn_stats_key_groups(B, Hq, Hkv, L, r0, Lr):
+    """Key groups of several 32-key tiles (the next tile of a group is prefetched while the
+    current one is used) and a shorter last group, with seeds inside and outside the region."""
+    announce(f"attn stats key groups B{B} Hq{Hq} Hkv{Hkv} L{L} r0 {r0} Lr {Lr}")
+    a = synth.attn_inputs("tiny", seed=L + Hq, max_seeds=40, B=B, Hq=Hq, Hkv=Hkv, L=L, d=128,
+                          dtype="bf16", prompt=0, unmasked_gen=L, n_seeds=40)
+    rng = np.random.default_rng(Lr)
+    masked = (rng.integers(0, 2, (B, Lr))).astype(np.uint8)
+    drafted = (rng.integers(0, 8, (B, Lr)) == 0).astype(np.uint8)
+    _stats_case(a, r0, masked, drafted)
+
+
+def test_attn_stats_workspace_checked():
+    """A caller workspace smaller than the launch needs, or of the wrong dtype, is refused
+    before anything is enqueued."""
+    announce("attn stats workspace checks")
+    a = synth.stats_inputs("llada", seed=0)
+    t = {k: a[k].cuda() for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx", "n_seed")}
+    _, lse = cover.cover_attn_fwd(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
+                                  t["seed_idx"], t["n_seed"])
+    m, d = a["masked"].cuda(), a["drafted"].cuda()
+    B, Hq, _, _ = a["q"].shape
+    need = cover.attn_stats_workspace(B, Hq, m.shape[1])
+    args = (t["q"], t["k_live"], t["k_cache"], t["seed_idx"], t["n_seed"], lse, m, d, a["r0"])
+    with pytest.raises(ValueError):
+        cover.cover_attn_stats(*args, workspace=torch.empty(need - 1, device="cuda"))
+    with pytest.raises(ValueError):
+        cover.cover_attn_stats(*args, workspace=torch.empty(need, device="cuda", dtype=torch.float64))
+    d_in, d_out = cover.cover_attn_stats(*args, workspace=torch.empty(need, device="cuda"))
+    r_in, r_out = cover.cover_attn_stats(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(d_in, r_in) and torch.equal(d_out, r_out)
+
+
 @pytest.mark.parametrize("name", ["llada", "dream"])
 def test_attn_stats_workload(name):
     """The generated block of the LLaDA-8B and Dream-7B layer shapes: 256 region positions,
