@@ -260,6 +260,31 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
  */
 int64_t cover_attn_stats_workspace(int32_t B, int32_t Hq, int32_t Lr);
 
+/* Floats of the library's own per-GPU workspace behind cover_attn_stats_noalloc (4 MiB). */
+#define COVER_STATS_SCRATCH_FLOATS (1 << 20)
+
+/*
+ * cover_attn_stats_noalloc -- cover_attn_stats without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation).  Same arguments, results and checks as cover_attn_stats, except
+ * that the partial sums go to a fixed array inside the library: COVER_STATS_SCRATCH_FLOATS
+ * floats on each GPU the library runs on, held until the process ends (its device address is
+ * looked up on the first call on each GPU; nothing is allocated, by this call or any other).
+ * Every call on one GPU shares that array and the work it enqueues reads back only what the
+ * same call wrote, so calls that run one after another (on one stream, or ordered by events)
+ * are independent; calls that can overlap on one GPU (different streams with no ordering)
+ * race on the array and give unspecified results.
+ * Returns COVER_ERR_UNSUPPORTED when cover_attn_stats_workspace(B, Hq, Lr) exceeds
+ * COVER_STATS_SCRATCH_FLOATS (for instance B * Hq > 256 at Lr = 2048, or B * Hq > 1024 at
+ * Lr = 512), before anything is enqueued; COVER_ERR_HIP if the array's address cannot be
+ * obtained.
+ */
+cover_status cover_attn_stats_noalloc(const void* q, const void* k_live, const void* k_cache,
+                                      const int32_t* seed_idx, const int32_t* n_seed,
+                                      const float* lse, const uint8_t* masked,
+                                      const uint8_t* drafted, float* d_in, float* d_out,
+                                      const cover_stats_desc* desc, hipStream_t stream);
+
 /*
  * Block-query attention description: the attention problem of cover_attn_fwd (same fields
  * and stride rules, with attn.L the number of keys; q and out hold Lq rows at the q strides)

@@ -20,7 +20,8 @@ COVER_MAX_L = 65536
 COVER_MAX_LR = 16384
 COVER_RECT_RECORD = 68
 
-EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_attn_stats_workspace",
+EXPORTED = ("cover_attn_fwd", "cover_attn_rect", "cover_attn_stats", "cover_attn_stats_noalloc",
+            "cover_attn_stats_workspace",
             "cover_debug_status", "cover_decode_update",
             "cover_select_seeds", "cover_status_str", "cover_token_sample", "cover_token_stats",
             "cover_version")
@@ -106,6 +107,9 @@ def lib():
         L.cover_token_sample.restype = ctypes.c_int
         L.cover_attn_stats.argtypes = [P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(StatsDesc), P]
         L.cover_attn_stats.restype = ctypes.c_int
+        L.cover_attn_stats_noalloc.argtypes = [P, P, P, P, P, P, P, P, P, P,
+                                               ctypes.POINTER(StatsDesc), P]
+        L.cover_attn_stats_noalloc.restype = ctypes.c_int
         L.cover_attn_stats_workspace.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
         L.cover_attn_stats_workspace.restype = ctypes.c_int64
         L.cover_status_str.argtypes = [ctypes.c_int]
@@ -394,6 +398,37 @@ def cover_attn_stats(q, k_live, k_cache, seed_idx, n_seed, lse, masked, drafted,
                                 _ptr(d_out), _ptr(workspace), ctypes.byref(desc), _stream(stream))
     if st != COVER_OK:
         raise CoverError(st, "cover_attn_stats")
+    return d_in, d_out
+
+
+COVER_STATS_SCRATCH_FLOATS = 1 << 20
+
+
+def cover_attn_stats_noalloc(q, k_live, k_cache, seed_idx, n_seed, lse, masked, drafted,
+                             r0: int, d_in, d_out, scale: float = 0.0, stream=None):
+    """cover_attn_stats with the library's own per-GPU workspace: nothing is allocated, so the
+    outputs d_in, d_out (contiguous fp32 [B, Lr]) are the caller's."""
+    B, Hq, L, d = q.shape
+    Lr = masked.shape[1]
+    for t in (k_live, k_cache):
+        if t.shape != k_live.shape or t.stride() != k_live.stride() or t.dtype != q.dtype:
+            raise ValueError("k_live and k_cache need equal shape, strides and dtype")
+    for t in (masked, drafted):
+        if t.shape != (B, Lr) or t.dtype != torch.uint8 or not t.is_contiguous():
+            raise ValueError("masked / drafted must be contiguous uint8 [B, Lr]")
+    if lse.shape != (B, Hq, L) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be contiguous fp32 [B, Hq, L]")
+    for t in (d_in, d_out):
+        if t.shape != (B, Lr) or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("d_in / d_out must be contiguous fp32 [B, Lr]")
+    max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+    desc = StatsDesc(attn_desc(q, k_live, max_seeds, scale), int(r0), int(Lr))
+    st = lib().cover_attn_stats_noalloc(_ptr(q), _ptr(k_live), _ptr(k_cache), _ptr(seed_idx),
+                                        _ptr(n_seed), _ptr(lse), _ptr(masked), _ptr(drafted),
+                                        _ptr(d_in), _ptr(d_out), ctypes.byref(desc),
+                                        _stream(stream))
+    if st != COVER_OK:
+        raise CoverError(st, "cover_attn_stats_noalloc")
     return d_in, d_out
 
 

@@ -160,11 +160,19 @@ int64_t cover_attn_stats_workspace(int32_t B, int32_t Hq, int32_t Lr) {
   return cover::stats_workspace_floats(B, Hq, Lr);
 }
 
-cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
-                              const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
-                              const uint8_t* masked, const uint8_t* drafted,
-                              float* d_in, float* d_out, float* workspace,
-                              const cover_stats_desc* desc, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks shared by cover_attn_stats and cover_attn_stats_noalloc: fills `a` (all
+// but the workspace) and returns COVER_OK, or the error to return before anything is enqueued.
+// *empty is set for a valid call with nothing to do.
+cover_status prepare_stats(const void* q, const void* k_live, const void* k_cache,
+                           const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
+                           const uint8_t* masked, const uint8_t* drafted, float* d_in,
+                           float* d_out, const cover_stats_desc* desc, cover::StatsArgs& a,
+                           bool* empty) {
+  *empty = false;
   if (!desc) return COVER_ERR_INVALID;
   const cover_attn_desc& D = desc->attn;
   const int32_t r0 = desc->r0, Lr = desc->Lr;
@@ -177,7 +185,10 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
   if (D.dtype != COVER_BF16) return COVER_ERR_UNSUPPORTED;
   if (D.d != 64 && D.d != 128) return COVER_ERR_UNSUPPORTED;
   if (D.L > COVER_MAX_L || Lr > COVER_STATS_MAX_LR) return COVER_ERR_UNSUPPORTED;
-  if (D.B == 0 || Lr == 0) return COVER_OK;
+  if (D.B == 0 || Lr == 0) {
+    *empty = true;
+    return COVER_OK;
+  }
   const void* tensors[3] = {q, k_live, k_cache};
   for (const void* t : tensors)
     if (!t || !aligned(t, 16)) return COVER_ERR_INVALID;
@@ -188,25 +199,65 @@ cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_c
   if (D.max_seeds > 0 && (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4)))
     return COVER_ERR_INVALID;
   if (!lse || !aligned(lse, 4) || !masked || !drafted) return COVER_ERR_INVALID;
-  if (!d_in || !d_out || !workspace || !aligned(d_in, 4) || !aligned(d_out, 4) ||
-      !aligned(workspace, 4))
-    return COVER_ERR_INVALID;
-  cover::StatsArgs a;
+  if (!d_in || !d_out || !aligned(d_in, 4) || !aligned(d_out, 4)) return COVER_ERR_INVALID;
   a.q = q; a.k_live = k_live; a.k_cache = k_cache;
   a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
   a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
   a.lse = lse; a.masked = masked; a.drafted = drafted;
-  a.d_in = d_in; a.d_out = d_out; a.workspace = workspace;
+  a.d_in = d_in; a.d_out = d_out; a.workspace = nullptr;
   a.B = D.B; a.Hq = D.Hq; a.Hkv = D.Hkv; a.L = D.L; a.d = D.d; a.max_seeds = D.max_seeds;
   a.r0 = r0; a.Lr = Lr;
   a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);
   a.q_sb = D.q_sb; a.q_sh = D.q_sh; a.q_sl = D.q_sl;
   a.kv_sb = D.kv_sb; a.kv_sh = D.kv_sh; a.kv_sl = D.kv_sl;
+  return COVER_OK;
+}
+
+cover_status run_stats(const cover::StatsArgs& a, const cover_stats_desc* desc, hipStream_t stream) {
   if (cover::debug_enabled()) {
-    const hipError_t e = cover::launch_check_seeds(a.seed_idx, a.n_seed, D.B, D.max_seeds, D.L, stream);
+    const hipError_t e = cover::launch_check_seeds(a.seed_idx, a.n_seed, a.B, a.max_seeds,
+                                                   desc->attn.L, stream);
     if (e != hipSuccess) return COVER_ERR_HIP;
   }
   return hip_status(cover::launch_attn_stats(a, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+cover_status cover_attn_stats(const void* q, const void* k_live, const void* k_cache,
+                              const int32_t* seed_idx, const int32_t* n_seed, const float* lse,
+                              const uint8_t* masked, const uint8_t* drafted,
+                              float* d_in, float* d_out, float* workspace,
+                              const cover_stats_desc* desc, hipStream_t stream) {
+  cover::StatsArgs a;
+  bool empty;
+  const cover_status st = prepare_stats(q, k_live, k_cache, seed_idx, n_seed, lse, masked,
+                                        drafted, d_in, d_out, desc, a, &empty);
+  if (st != COVER_OK || empty) return st;
+  if (!workspace || !aligned(workspace, 4)) return COVER_ERR_INVALID;
+  a.workspace = workspace;
+  return run_stats(a, desc, stream);
+}
+
+cover_status cover_attn_stats_noalloc(const void* q, const void* k_live, const void* k_cache,
+                                      const int32_t* seed_idx, const int32_t* n_seed,
+                                      const float* lse, const uint8_t* masked,
+                                      const uint8_t* drafted, float* d_in, float* d_out,
+                                      const cover_stats_desc* desc, hipStream_t stream) {
+  cover::StatsArgs a;
+  bool empty;
+  const cover_status st = prepare_stats(q, k_live, k_cache, seed_idx, n_seed, lse, masked,
+                                        drafted, d_in, d_out, desc, a, &empty);
+  if (st != COVER_OK || empty) return st;
+  if (cover::stats_workspace_floats(a.B, a.Hq, a.Lr) > COVER_STATS_SCRATCH_FLOATS)
+    return COVER_ERR_UNSUPPORTED;
+  // the library's own per-GPU array (looked up once per device; nothing is allocated)
+  float* scratch = nullptr;
+  if (cover::stats_scratch(&scratch) != hipSuccess || !scratch) return COVER_ERR_HIP;
+  a.workspace = scratch;
+  return run_stats(a, desc, stream);
 }
 
 cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_live,

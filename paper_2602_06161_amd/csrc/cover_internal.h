@@ -116,6 +116,9 @@ hipError_t launch_attn_stats(const StatsArgs& a, hipStream_t stream);
 // floats that launch uses
 void stats_key_groups(int B, int Hq, int Lr, int* tpg, int* kg);
 int64_t stats_workspace_floats(int B, int Hq, int Lr);
+// device address of the attention-mass kernels' own static scratch array on the current GPU
+// (COVER_STATS_SCRATCH_FLOATS floats), looked up once per device
+hipError_t stats_scratch(float** ptr);
 hipError_t launch_decode_update(const UpdateArgs& a, hipStream_t stream);
 hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream);  // bf16, d = 128
 

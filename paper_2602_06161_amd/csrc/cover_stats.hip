@@ -19,6 +19,8 @@
 // and averages over heads; every sum runs in a fixed order, so the results do not depend on
 // scheduling.
 #include <hip/hip_runtime.h>
+
+#include <mutex>
 #include <stdint.h>
 
 #include "cover.h"
@@ -353,6 +355,34 @@ hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream) {
   p.bf16 = a.bf16;
   hipLaunchKernelGGL(cover_token_stats_kernel, dim3((unsigned)a.R), dim3(kTokThreads), 0, stream, p);
   return hipGetLastError();
+}
+
+// The workspace of cover_attn_stats_noalloc: one array per GPU, held until the process ends.
+// Host code never passes `scratch` itself to a kernel (in host code the name stands for a
+// host-side shadow, not a device address); it passes the address hipGetSymbolAddress gives
+// for the current device.
+static __device__ __align__(256) float scratch[COVER_STATS_SCRATCH_FLOATS];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t stats_scratch(float** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 void stats_key_groups(int B, int Hq, int Lr, int* tpg, int* kg_out) {

@@ -164,6 +164,44 @@ def test_attn_stats_rejects_bad_descriptors(kw, r0, Lr, expect):
     assert _stats(cover.StatsDesc(_good(**kw), r0, Lr)) == expect
 
 
+def _stats_na(desc, lse=FAKE, d_in=FAKE):
+    p = lambda x: None if x is None else ctypes.c_void_p(x)
+    return cover.lib().cover_attn_stats_noalloc(p(FAKE), p(FAKE), p(FAKE), p(FAKE), p(FAKE),
+                                                p(lse), p(FAKE), p(FAKE), p(d_in), p(FAKE),
+                                                None if desc is None else ctypes.byref(desc), None)
+
+
+@pytest.mark.parametrize("kw,r0,Lr,expect", [
+    (dict(), -1, 8, cover.COVER_ERR_INVALID),
+    (dict(), 60, 8, cover.COVER_ERR_INVALID),
+    (dict(dtype=cover.COVER_F32), 0, 8, cover.COVER_ERR_UNSUPPORTED),
+    (dict(Hkv=3), 0, 8, cover.COVER_ERR_INVALID),
+    (dict(), 0, 0, cover.COVER_OK),
+    (dict(L=2048, Hq=257, Hkv=257), 0, 2048, cover.COVER_ERR_UNSUPPORTED),  # beyond its array
+    (dict(L=512, Hq=1025, Hkv=1025), 0, 512, cover.COVER_ERR_UNSUPPORTED),
+])
+def test_attn_stats_noalloc_rejects_before_any_gpu_call(kw, r0, Lr, expect):
+    # every one of these returns before the library touches the GPU (there is none here)
+    assert _stats_na(cover.StatsDesc(_good(**kw), r0, Lr)) == expect
+
+
+def test_attn_stats_noalloc_rejects_missing_buffers():
+    good = cover.StatsDesc(_good(), 0, 8)
+    assert _stats_na(None) == cover.COVER_ERR_INVALID
+    assert _stats_na(good, lse=None) == cover.COVER_ERR_INVALID
+    assert _stats_na(good, d_in=None) == cover.COVER_ERR_INVALID
+
+
+def test_attn_stats_workspace_sizes():
+    ws = cover.lib().cover_attn_stats_workspace
+    assert ws(1, 32, 256) == 32 * 9 * 256        # 8 key tiles, one per group
+    assert ws(2, 4, 1100) == 8 * 19 * 1100       # 35 tiles in 18 groups
+    assert ws(1, 256, 2048) == cover.COVER_STATS_SCRATCH_FLOATS
+    assert ws(0, 4, 100) == 0 and ws(-1, 4, 100) == -1
+    for B, Hq, Lr in [(1, 1, 1), (3, 7, 2048), (8, 32, 512), (1, 300, 33)]:
+        assert ws(B, Hq, Lr) <= B * Hq * (1 + (Lr + 31) // 32) * Lr  # the header's bound
+
+
 def test_attn_stats_rejects_missing_buffers():
     good = cover.StatsDesc(_good(), 0, 8)
     assert _stats(None) == cover.COVER_ERR_INVALID
