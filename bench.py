@@ -39,7 +39,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = ("paper_2602_06161_amd/csrc/cover_attn_w4.hip",)
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_llada_hbm_traffic.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_{workload}_hbm_traffic.md")
 
 
 def kernel_source_hash() -> str:
@@ -51,11 +51,12 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per attention launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+    """HBM bytes per attention launch from the committed rocprofv3 counter summary of this
+    workload, if it was taken on the current kernel source; else None."""
+    path = TRAFFIC_SUMMARY.format(workload=workload)
+    if not os.path.exists(path):
         return None
-    text = open(TRAFFIC_SUMMARY).read()
+    text = open(path).read()
     m = re.search(r"^traffic_bytes_per_launch:\s*(\d+)\s+workload:\s*(\w+)\s+source:\s*(\w+)",
                   text, flags=re.M)
     if not m or m.group(2) != workload or m.group(3) != kernel_source_hash():
@@ -73,6 +74,17 @@ def main() -> int:
     ap.add_argument("--only", choices=["attn", "select"], default=None)
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-phase-timing", action="store_true",
+                    help="skip the shader-clock / phase leg (a child process running the timing "
+                         "build of the attention kernel once)")
+    ap.add_argument("--calibrate-mfma", action="store_true",
+                    help="run the pure-MFMA calibration kernel of the timing build (one "
+                         "workgroup of four waves per CU, bf16 32x32x16 MFMAs only) K times; "
+                         "the reference for the MFMA counters")
+    ap.add_argument("--phase-timing", action="store_true",
+                    help="run the attention kernel of the timing build of the library "
+                         "(lib/libcover_timing.so) once after warm-up and print where a "
+                         "workgroup's cycles go, and the shader clock under load")
     ap.add_argument("--kernel", choices=["token_stats", "token_sample", "attn_stats",
                                          "decode_update"], default=None)
     ap.add_argument("--lm-scale", type=float, default=8.0,
@@ -116,6 +128,10 @@ def main() -> int:
         print(json.dumps({"copy_mib": args.copy_mib, "launches": args.steps}))
         return 0
 
+    if args.phase_timing:
+        return bench_phase_timing(args, dev, stream)
+    if args.calibrate_mfma:
+        return bench_calibrate_mfma(args, dev, stream)
     if args.kernel:
         return bench_producer(args, dev, stream)
     if args.workload == "block":
@@ -254,10 +270,32 @@ def main() -> int:
             "algorithmic_flops_per_launch": flops,
         },
     }
+    if not args.no_phase_timing:
+        ph = phase_leg(args.workload)
+        if ph is not None:
+            rec["sclk_ghz_under_load"] = ph["sclk_ghz_median"]
+            rec["phase_cycles_median"] = ph["cycles_median"]
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(a, flops)
     print(json.dumps(rec))
     return 0
+
+
+def phase_leg(workload: str):
+    """The timing build of the attention kernel, run once after warm-up in a child process
+    (`--phase-timing`): the shader clock under load and the per-phase cycle medians.  None
+    (with a note on stderr) if that run fails."""
+    import subprocess
+
+    cmd = [sys.executable, os.path.abspath(__file__), "--phase-timing", "--workload", workload,
+           "--warmup", "5"]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+    lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
+    if r.returncode != 0 or not lines:
+        print(f"bench.py: phase-timing leg failed (rc {r.returncode}): {r.stderr[-400:]}",
+              file=sys.stderr)
+        return None
+    return json.loads(lines[-1])
 
 
 def bench_producer(args, dev, stream) -> int:
@@ -507,6 +545,109 @@ def bench_full_step(args, dev, stream, loop: bool = False) -> int:
         "attn_flops_share": round(flops_attn / flops_step, 4),
         "step_tflops": round(flops_step / (step_ms * 1e-3) / 1e12, 1),
         "dtype": "bf16", "data": "synthetic (random-init weights N(0, 0.02), random token ids)"}))
+    return 0
+
+
+def bench_calibrate_mfma(args, dev, stream) -> int:
+    """K launches of the pure-MFMA calibration kernel (256 workgroups of 4 waves, each wave
+    4 x 8192 MFMAs of 32x32x16 bf16) between two events; prints its achieved TFLOP/s."""
+    import ctypes
+
+    import torch
+    from paper_2602_06161_amd import cover
+    from paper_2602_06161_amd.build import LIB_TIMING
+
+    cover.use_library(LIB_TIMING)
+    grid, iters = 256, 8192
+    out = torch.empty(grid * 256, device=dev, dtype=torch.float32)
+    fn = cover.lib().cover_calib_mfma
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    run = lambda: fn(cover._ptr(out), grid, iters, cover._stream(stream))
+    for _ in range(max(1, args.warmup)):
+        if run() != 0:
+            raise RuntimeError("calibration launch failed")
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / args.steps
+    flops = grid * 4 * 4 * iters * 32768
+    print(json.dumps({"calibrate_mfma": "256 workgroups x 4 waves, 4 x 8192 bf16 32x32x16 MFMAs per wave",
+                      "flops_per_launch": flops, "us_per_launch": round(us, 3),
+                      "tflops": round(flops / us / 1e6, 1),
+                      "frac_of_2516_6": round(flops / us / 1e6 / PEAK_BF16_TFLOPS, 4)}))
+    return 0
+
+
+def bench_phase_timing(args, dev, stream) -> int:
+    """Per-phase cycle counts of cover_attn_w4_kernel from its timing build: every wave's
+    shader-clock stamps at fixed points (see the slot list in the kernel source), summarised
+    as medians over all waves of all workgroups, per-step medians, the slowest workgroup, and
+    the shader clock (stamps over the 100-MHz real-time counter)."""
+    import numpy as np
+    import torch
+    from paper_2602_06161_amd import cover, synth
+    from paper_2602_06161_amd.build import LIB_TIMING
+
+    cover.use_library(LIB_TIMING)
+    a = synth.attn_inputs(args.workload, seed=args.seed)
+    c = a["cfg"]
+    t = {k: a[k].to(dev) for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx",
+                                   "n_seed")}
+    attn = cover.PreparedAttn(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
+                              t["seed_idx"], t["n_seed"], stream=stream)
+    for _ in range(args.warmup):
+        attn()
+    torch.cuda.synchronize()
+    attn()
+    torch.cuda.synchronize()
+    WG, W, S = 4096, 4, 96
+    buf = np.zeros(WG * W * S, dtype=np.uint64)
+    rc = cover.lib().cover_attn_timing_read(buf.ctypes.data_as(__import__("ctypes").c_void_p),
+                                            __import__("ctypes").c_int64(buf.size))
+    if rc != 0:
+        raise RuntimeError(f"cover_attn_timing_read failed ({rc})")
+    n_qt = -(-c.L // 128)
+    nwg = min(WG, c.B * c.Hq * n_qt)
+    T = buf.reshape(WG, W, S)[:nwg].astype(np.int64)
+    n_it = -(-c.L // 64)
+    med = lambda x: float(np.median(x))
+    ghz = (T[:, :, 94] - T[:, :, 0]) / ((T[:, :, 95] - T[:, :, 1]) / 100e6) / 1e9
+    last_top = 6 + min(n_it - 2, 63)
+    phases = {
+        "q_k0_landed": T[:, :, 2] - T[:, :, 0],
+        "seed_bitmap": T[:, :, 3] - T[:, :, 2],
+        "q_to_registers": T[:, :, 4] - T[:, :, 3],
+        "s0_and_maxima": T[:, :, 5] - T[:, :, 4],
+        "first_step_wait": T[:, :, 6] - T[:, :, 5],
+        "steps": T[:, :, last_top] - T[:, :, 6],
+        "to_last_stage": T[:, :, 70] - T[:, :, last_top],
+        "last_stage": T[:, :, 71] - T[:, :, 70],
+        "drain_loads": T[:, :, 72] - T[:, :, 71],
+        "merge_exchange": T[:, :, 73] - T[:, :, 72],
+        "finish_rows": T[:, :, 74] - T[:, :, 73],
+        "issue_stores": T[:, :, 75] - T[:, :, 74],
+        "stores_complete": T[:, :, 94] - T[:, :, 75],
+        "total": T[:, :, 94] - T[:, :, 0],
+    }
+    steps = [med(T[:, :, 7 + i] - T[:, :, 6 + i]) for i in range(min(n_it - 2, 63))]
+    tot = phases["total"].max(axis=1)
+    slow = int(np.argmax(tot))
+    rec = {
+        "phase_timing": f"{args.workload}: B={c.B} Hq={c.Hq} Hkv={c.Hkv} L={c.L} d={c.d}",
+        "workgroups": nwg,
+        "sclk_ghz_median": round(med(ghz), 3),
+        "sclk_ghz_min": round(float(ghz.min()), 3),
+        "cycles_median": {k: med(v) for k, v in phases.items()},
+        "cycles_slowest_workgroup": {k: float(v[slow].max()) for k, v in phases.items()},
+        "slowest_workgroup": slow,
+        "step_cycles_median": steps,
+    }
+    print(json.dumps(rec))
     return 0
 
 

@@ -17,6 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "lib", "libcover.so")
+# the same library with the attention kernel's phase timestamps compiled in (measurement only)
+LIB_TIMING = os.path.join(PKG, "lib", "libcover_timing.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC") or shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
@@ -42,9 +44,17 @@ SOURCES = {
 }
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(OBJDIR, src + ".o")
-    cmd = [HIPCC, *COMMON, *SOURCES[src], "-c", os.path.join(CSRC, src), "-o", obj]
+# sources compiled a second time, with these flags, for LIB_TIMING
+TIMING = {"cover_attn_w4.hip": ["-DCOVER_ATTN_TIMING=1"]}
+# sources of LIB_TIMING only (the MFMA-counter calibration kernel)
+TIMING_ONLY = {"cover_calib.hip": []}
+
+
+def _compile(src: str, timing: bool = False) -> str:
+    obj = os.path.join(OBJDIR, src + (".timing.o" if timing else ".o"))
+    flags = SOURCES[src] if src in SOURCES else TIMING_ONLY[src]
+    extra = TIMING.get(src, []) if timing else []
+    cmd = [HIPCC, *COMMON, *flags, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
@@ -54,16 +64,21 @@ def _compile(src: str) -> str:
 def build(verbose: bool = True) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     os.makedirs(os.path.dirname(LIB), exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    if verbose:
-        print(f"built {LIB}", file=sys.stderr)
+    jobs = ([(src, False) for src in SOURCES] + [(src, True) for src in TIMING]
+            + [(src, True) for src in TIMING_ONLY])
+    with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
+        built = dict(zip(jobs, ex.map(lambda j: _compile(*j), jobs)))
+    plain = [built[(src, False)] for src in SOURCES]
+    timed = [built[(src, src in TIMING)] for src in SOURCES] + [built[(src, True)] for src in TIMING_ONLY]
+    for lib, objs in ((LIB, plain), (LIB_TIMING, timed)):
+        tmp = lib + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        os.replace(tmp, lib)
+        if verbose:
+            print(f"built {lib}", file=sys.stderr)
     return LIB
 
 

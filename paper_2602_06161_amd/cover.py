@@ -80,16 +80,26 @@ def attn_stats_workspace(B: int, Hq: int, Lr: int) -> int:
 
 
 _lib = None
+_lib_path = LIB
+
+
+def use_library(path: str) -> None:
+    """Load the library from `path` instead of libcover.so (the in-tree timing build of the
+    same sources, for measurements).  Must come before the first call."""
+    global _lib_path
+    if _lib is not None and path != _lib_path:
+        raise RuntimeError("the COVER library is already loaded")
+    _lib_path = path
 
 
 def lib():
     """Load libcover.so (built in-tree); raise if it is missing."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            raise RuntimeError(f"COVER HIP library not built ({LIB}); run "
+        if not os.path.exists(_lib_path):
+            raise RuntimeError(f"COVER HIP library not built ({_lib_path}); run "
                                "`python -m paper_2602_06161_amd.build` or __graft_entry__.build()")
-        L = ctypes.CDLL(LIB)
+        L = ctypes.CDLL(_lib_path)
         P = ctypes.c_void_p
         L.cover_attn_fwd.argtypes = [P, P, P, P, P, P, P, P, P, ctypes.POINTER(AttnDesc), P]
         L.cover_attn_fwd.restype = ctypes.c_int

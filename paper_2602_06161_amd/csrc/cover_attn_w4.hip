@@ -192,6 +192,35 @@ struct IC {
   static constexpr int value = N;
 };
 
+// Phase timing (a separate build of the library, -DCOVER_ATTN_TIMING=1, used only to measure
+// where a workgroup's time goes): lane 0 of every wave of the first kTimeWG logical
+// workgroups stores the shader-clock counter at fixed points of the kernel, plus the 100-MHz
+// real-time counter at the start and the end (their ratio is the shader clock under load).
+// Slots: 0 start, 1 real time at start, 2 Q and K(0) landed, 3 seed bitmap built, 4 Q in
+// registers, 5 S(0) and the reference maxima, 6 + i top of step i (after its barrier, i < 64),
+// 70 last stage after its barrier, 71 last stage done, 72 all loads landed, 73 partner tile
+// readable, 74 rows finished, 75 stores issued, 94 end, 95 real time at the end.
+#ifndef COVER_ATTN_TIMING
+#define COVER_ATTN_TIMING 0
+#endif
+#if COVER_ATTN_TIMING
+constexpr int kTimeWG = 4096, kTimeSlots = 96;
+__device__ uint64_t g_attn_times[kTimeWG * kWaves * kTimeSlots];
+#define COVER_TSTAMP(slot)                                                                      \
+  do {                                                                                          \
+    if (li < kTimeWG && lane == 0 && (slot) < kTimeSlots)                                       \
+      g_attn_times[((int64_t)li * kWaves + wave) * kTimeSlots + (slot)] = __builtin_readcyclecounter(); \
+  } while (0)
+#define COVER_TREAL(slot)                                                                       \
+  do {                                                                                          \
+    if (li < kTimeWG && lane == 0)                                                              \
+      g_attn_times[((int64_t)li * kWaves + wave) * kTimeSlots + (slot)] = __builtin_amdgcn_s_memrealtime(); \
+  } while (0)
+#else
+#define COVER_TSTAMP(slot) do {} while (0)
+#define COVER_TREAL(slot) do {} while (0)
+#endif
+
 __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params4 p) {
   // Three K and three V stage buffers; Q of the workgroup on its way to registers (at the end:
   // the live key rows of the seed rows' diagonals); the seed list, the seed bitmap of the
@@ -222,6 +251,8 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   // ---- workgroup -> (b, h, query tile); consecutive logical tiles share an XCD ------------
   int li = blockIdx.x;
   if (p.xcd_slots > 0) li = (li & 7) * p.xcd_slots + (li >> 3);
+  COVER_TSTAMP(0);
+  COVER_TREAL(1);
   const int qt = li % p.n_qt;
   const int bh = li / p.n_qt;
   const int h = bh % p.Hq, b = bh / p.Hq;
@@ -301,6 +332,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   // K(1) are first needed at the top of step 0)
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
+  COVER_TSTAMP(2);
   ld_live(vbuf(0), vlb, true, 0);
   ld_live(kbuf(1), klb, false, clamp_stage(1));
   ld_live(vbuf(1), vlb, true, clamp_stage(1));
@@ -322,6 +354,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     if ((unsigned)j < (unsigned)L) mark(j);
   }
   __syncthreads();
+  COVER_TSTAMP(3);
   auto is_seed = [&](int j) __attribute__((always_inline)) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
 
   // Lane l holds the seed flags of stages 64 l .. 64 l + 63 (two words); a stage's flag is
@@ -452,6 +485,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       asm volatile("ds_read_b128 %0, %1" : "=a"(qa[t][ks]) : "v"(lds_u32v((lds_t*)sQ + k_off(r, 2 * ks + hl))));
     }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the Q reads above (not tracked by the compiler)
+  COVER_TSTAMP(4);
 
   // ---- per-lane LDS read addresses (relative to a stage buffer) ---------------------------
   uint32_t kaddr[kKS];
@@ -649,6 +683,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     const float mt = swap_max(lane_max(sA[t])) * p.c2;
     m[t] = mt > kInitMax ? mt : kInitMax;
   }
+  COVER_TSTAMP(5);
 
   // ---- steady state --------------------------------------------------------------------------
   // Step i (i < n_it - 1): wait for this wave's loads of K(i+1), V(i) (issued two steps
@@ -712,6 +747,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     vgr += stage_bytes;
     __builtin_amdgcn_s_waitcnt(kWaitStep);
     __builtin_amdgcn_s_barrier();
+    COVER_TSTAMP(6 + (i < 64 ? i : 63));
     // the stages loaded in the previous step, K(i+2) and V(i+1), get their seed / ragged
     // rows now: after the wait (which would otherwise also wait for the previous step's
     // loads), before this step's loads (so the wait at the top of the next step covers them);
@@ -751,15 +787,18 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads));
     }
     __builtin_amdgcn_s_barrier();
+    COVER_TSTAMP(70);
     bf16x8 pk[2][2];
     bad |= softmax(sc, pk, m);
     const int vb = last % 3;
     pv(vbuf(0) + (vb == 0 ? 0 : (vb == 1 ? (int)(vbuf(1) - vbuf(0)) : (int)(vbuf(2) - vbuf(0)))), pk, IC<4>{});
     if (block_seeded) s_live = live_score();  // the key rows' load overlapped the last stage
+    COVER_TSTAMP(71);
   }
   if (bad) atomicOr(&sbad, 1u);
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // the loads past the end (their buffers are reused)
   __syncthreads();
+  COVER_TSTAMP(72);
 
   // ---- exact pass (only if some row's scores outgrew its first-stage maximum by 2^24) ----
   if (sbad) {
@@ -819,6 +858,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
   sML[(wave * 2 + 1) * 64 + lane] = l_tot1;
   if (block_seeded) load_diag_v();  // the seed rows' live values, for the finish
   __syncthreads();
+  COVER_TSTAMP(73);
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
   // d = 32 db + 8 (j / 4) + 4 hl + j % 4.
   bf16x4 outv[kDB * 4];
@@ -859,6 +899,7 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
   };
   if (block_seeded) finish(IC<1>{}); else finish(IC<0>{});
+  COVER_TSTAMP(74);
   if (p.lse && hl == 0 && qd0 + l32 < L)
     p.lse[((int64_t)b * p.Hq + h) * L + qd0 + l32] = (mm_out + __builtin_amdgcn_logf(ltot_out)) * kLn2;
   // Rows go out through this wave's own 8-KiB tile in the Q area (idle since Q went to
@@ -890,9 +931,25 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       if (qd0 + row < L) *(u32x4*)(obase + (int64_t)(qd0 + row) * p.q_sl + ch * 8) = ov[it];
     }
   }
+  COVER_TSTAMP(75);
+#if COVER_ATTN_TIMING
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores complete
+  COVER_TSTAMP(94);
+  COVER_TREAL(95);
+#endif
 }
 
 }  // namespace
+
+#if COVER_ATTN_TIMING
+// Copies the timing slots of the last launches (layout [workgroup][wave][slot], 4096 x 4 x 96
+// values) to host memory; waits for the device.  Only in the timing build of the library.
+extern "C" int cover_attn_timing_read(uint64_t* host, int64_t n) {
+  const int64_t cap = (int64_t)kTimeWG * kWaves * kTimeSlots;
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(g_attn_times), sizeof(uint64_t) * (n < cap ? n : cap),
+                                  0, hipMemcpyDeviceToHost);
+}
+#endif
 
 hipError_t launch_attn_bf16_w4(const AttnArgs& a, hipStream_t stream) {
   Params4 p;

@@ -129,6 +129,32 @@ def test_nonseed_cache_rows_are_never_read():
     assert torch.equal(out, out2) and torch.equal(lse, lse2)
 
 
+def test_out_of_range_entries_are_ignored():
+    announce("bf16 seed lists with entries outside [0, L); a row with none inside")
+    L = 200
+    a = _custom(16, 2, 4, 2, L, 128, 0, max_seeds=8)
+    si = np.array([[-7, 5, L, 130, L + 1000, 64, -1, 199],
+                   [-1, L, L + 3, -100, 0, 0, 0, 0]], np.int32)
+    ns = np.array([8, 4], np.int32)
+    kept = [[5, 130, 64, 199], []]
+    a["seed_idx"], a["n_seed"] = torch.from_numpy(si), torch.from_numpy(ns)
+    kc, vc = a["k_cache"].clone(), a["v_cache"].clone()
+    for b in range(2):   # cache rows that are not seeds must never be read
+        non = np.setdiff1d(np.arange(L), kept[b])
+        kc[b][:, non] = float("nan")
+        vc[b][:, non] = float("inf")
+    a["k_cache"], a["v_cache"] = kc, vc
+    out, lse = _run(a)
+    assert torch.isfinite(out.float()).all()
+    ref_in = dict(a)
+    rsi = np.full((2, 4), -1, np.int32)
+    rsi[0] = kept[0]
+    ref_in["seed_idx"] = torch.from_numpy(rsi)
+    ref_in["n_seed"] = torch.tensor([4, 0], dtype=torch.int32)
+    ref, lref = _oracle(ref_in)
+    check_attn(out, lse, ref, lref, torch.bfloat16, "out-of-range entries")
+
+
 def test_seed_row_ignores_its_own_cached_kv():
     announce("bf16 perturb one seed's own cached K/V")
     a = _custom(7, 1, 2, 2, 256, 128, 9)

@@ -19,13 +19,19 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_traffic_figure_tracks_the_kernel_source():
-    text = open(bench.TRAFFIC_SUMMARY).read()
-    m = re.search(r"^traffic_bytes_per_launch:\s*(\d+)\s+workload:\s*(\w+)\s+source:\s*(\w+)",
-                  text, flags=re.M)
-    assert m, "the profile must carry its machine-readable line"
-    got = bench.measured_traffic(m.group(2))
-    if m.group(3) == bench.kernel_source_hash():
-        assert got == int(m.group(1))
-    else:
-        assert got is None
+    for w in ("llada", "dream", "batched"):
+        path = bench.TRAFFIC_SUMMARY.format(workload=w)
+        if not os.path.exists(path):
+            assert bench.measured_traffic(w) is None
+            continue
+        text = open(path).read()
+        m = re.search(r"^traffic_bytes_per_launch:\s*(\d+)\s+workload:\s*(\w+)\s+source:\s*(\w+)",
+                      text, flags=re.M)
+        assert m, "the profile must carry its machine-readable line"
+        assert m.group(2) == w
+        got = bench.measured_traffic(w)
+        if m.group(3) == bench.kernel_source_hash():
+            assert got == int(m.group(1))
+        else:
+            assert got is None
     assert bench.measured_traffic("no-such-workload") is None
