@@ -181,66 +181,108 @@ __global__ __launch_bounds__(kThreads, 2) void cover_attn_rect_kernel(const Rect
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
   float m = kInit, l = 0.0f;
 
-  for (int st = 0; st < n_st; ++st) {
+  // Two 32-key stages per pass (they are in the same group: groups start at multiples of
+  // four stages): two independent S^T chains, one softmax over both, and every LDS operand of
+  // the pass requested before its first MFMA (one LDS latency per pass).  The running max is
+  // raised lazily, once some row's scores exceed it by 2^8 (weights up to 256 stay exact
+  // enough in bf16 and far from fp32 overflow), so O is rarely rescaled; the first pass sets
+  // it while O and the sums are still zero.
+  constexpr float kLazy = 8.0f;
+  for (int st = 0; st < n_st; st += 2) {
     const int buf = st % kGroup;
     if (buf == 0) {
       if (st > 0) __syncthreads();  // every wave is done with the previous group
       load_group(st, min(kGroup, n_st - st));
       __syncthreads();
     }
+    const bool two = st + 1 < n_st;
     if (active) {
-      const lds_t* kb = (const lds_t*)sK[buf];
-      const lds_t* vb = (const lds_t*)sV[buf];
-      f32x16 s;
+      bf16x8 ka[2][kD / 16], va[2][2][kD / 32];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+      for (int kt = 0; kt < 2; ++kt) {
+        const lds_t* kb = (const lds_t*)sK[buf + (two ? kt : 0)];
+        const lds_t* vb = (const lds_t*)sV[buf + (two ? kt : 0)];
 #pragma unroll
-      for (int ks = 0; ks < kD / 16; ++ks) {
-        const bf16x8 a = *(const __attribute__((address_space(3))) bf16x8*)(kb + k_off(l32, 2 * ks + hl));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s, 0, 0, 0);
+        for (int ks = 0; ks < kD / 16; ++ks)
+          ka[kt][ks] = *(const __attribute__((address_space(3))) bf16x8*)(kb + k_off(l32, 2 * ks + hl));
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int db = 0; db < kD / 32; ++db) {
+            const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
+            va[kt][kk][db] = __builtin_bit_cast(
+                bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
+          }
       }
-      // register r holds key k0 + 8 (r / 4) + 4 hl + r % 4 of query row qrow
-      const int k0 = k_begin + st * kStage;
-      float mx = kInit;
+      f32x16 sc[2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + 8 * (r >> 2) + 4 * hl + (r & 3);
-        float t = s[r] * p.c2;
-        if (key >= k_end || (row_seed && key == pos)) t = -INFINITY;
-        s[r] = t;
-        mx = __builtin_fmaxf(mx, t);
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[kt][r] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < kD / 16; ++ks)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+          sc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kt][ks], qreg[ks], sc[kt], 0, 0, 0);
+      // register r of stage kt holds key k0 + 32 kt + 8 (r / 4) + 4 hl + r % 4 of row qrow
+      const int k0 = k_begin + st * kStage;
+      const bool edge = k0 + 2 * kStage > k_end;  // keys past the split's end (or no stage 2)
+      const bool diag = row_seed && pos >= k0 && pos < k0 + 2 * kStage;
+      float mx = kInit;
+      if (__builtin_amdgcn_ballot_w64(diag) != 0 || edge) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * kt + 8 * (r >> 2) + 4 * hl + (r & 3);
+            float t = sc[kt][r] * p.c2;
+            if (key >= k_end || (diag && key == pos)) t = -INFINITY;
+            sc[kt][r] = t;
+            mx = __builtin_fmaxf(mx, t);
+          }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            sc[kt][r] *= p.c2;
+            mx = __builtin_fmaxf(mx, sc[kt][r]);
+          }
       }
       mx = pair_max(mx);
-      const float mn = __builtin_fmaxf(m, mx);
-      if (__builtin_amdgcn_ballot_w64(mn > m)) {  // some row's max grew: rescale
+      if (st == 0) {
+        m = mx;
+      } else if (__builtin_amdgcn_ballot_w64(mx > m + kLazy)) {
+        const float mn = __builtin_fmaxf(m, mx);
         const float alpha = __builtin_amdgcn_exp2f(m - mn);
         l *= alpha;
 #pragma unroll
+        for (int db = 0; db < kD / 32; ++db) o[db] *= alpha;
+        m = mn;
+      }
+      bf16x8 pk[2][2];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pr = __builtin_amdgcn_exp2f(sc[kt][8 * kk + e] - m);
+            l += pr;
+            pk[kt][kk][e] = (__bf16)pr;
+          }
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
         for (int db = 0; db < kD / 32; ++db)
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[0][kk][db], pk[0][kk], o[db], 0, 0, 0);
+      if (two) {  // (a lone last stage: its second half is all masked, and its buffer stale)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int db = 0; db < kD / 32; ++db)
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[1][kk][db], pk[1][kk], o[db], 0, 0, 0);
       }
-      m = mn;
-      float pr[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        pr[r] = __builtin_amdgcn_exp2f(s[r] - m);
-        l += pr[r];
-      }
-      bf16x8 pk[2];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pk[kk][e] = (__bf16)pr[8 * kk + e];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int db = 0; db < kD / 32; ++db) {
-          const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
-          const bf16x8 va = __builtin_bit_cast(
-              bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pk[kk], o[db], 0, 0, 0);
-        }
     }
   }
 
