@@ -3,8 +3,10 @@
 // cover_token_stats_kernel: per row of the model's output logits, the log-probability of the
 // token currently placed there (u = -log p, Sec. 5.3), the maximum probability (the
 // confidence of Sec. 3) and the token attaining it.  One workgroup of 1024 threads per row;
-// HBM-bound: each thread streams 16-byte chunks with four loads in flight and keeps an
-// online (max, sum of exp, argmax) triple, merged across the workgroup at the end.
+// each thread streams 16-byte chunks with four loads in flight and keeps an online (max, sum
+// of exp) pair and the chunk where its max was last raised (the index inside it is found at
+// the end), merged across the workgroup.  The placed token and its logit are fetched at the
+// start by scalar loads, so no memory round trip is left for the end.
 //
 // cover_attn_stats_kernel + cover_attn_stats_reduce_kernel: the in/out attention masses of
 // Sec. 5.3 over a response region [r0, r0+Lr), from the last layer's corrected weights
@@ -34,7 +36,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) const u32x4 gu32x4;
 
 constexpr int kTokThreads = 1024;
-constexpr int kTokUnroll = 4;  // 16-byte loads in flight per thread
+constexpr int kTokUnroll = 4;  // 16-byte loads in flight per thread (more measured slower)
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kLn2 = 0.693147180559945309f;
 
@@ -46,7 +48,6 @@ struct TokParams {
   int32_t* argmax;
   int64_t row_stride_bytes;
   int V;
-  int bf16;
 };
 
 // (m, s, i): running max, sum of exp2((x - m) * log2e) over the elements seen, the smallest
@@ -69,63 +70,114 @@ __device__ __forceinline__ Acc merge(Acc a, Acc b) {
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fold the n (<= 8) values of one chunk, starting at element index j0, into acc
-__device__ __forceinline__ void fold(Acc& acc, const float* x, int n, int j0) {
-  float cm = x[0];
-  int ci = j0;
+// the N values of a 16-byte chunk
+template <bool BF>
+__device__ __forceinline__ void unpack(u32x4 v, float* x) {
+  if constexpr (BF) {
 #pragma unroll
-  for (int e = 1; e < 8; ++e)
-    if (e < n && x[e] > cm) { cm = x[e]; ci = j0 + e; }
-  if (cm > acc.m) {
-    acc.s = acc.s == 0.0f ? 0.0f : acc.s * __builtin_amdgcn_exp2f((acc.m - cm) * kLog2e);
-    acc.m = cm;
-    acc.i = ci;
+    for (int e = 0; e < 4; ++e) { x[2 * e] = bf_lo(v[e]); x[2 * e + 1] = bf_hi(v[e]); }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(v[e]);
   }
-  const float nm = -acc.m * kLog2e;
-  float add = 0.0f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e)
-    if (e < n) add += __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], kLog2e, nm));
-  acc.s += add;
 }
 
+// Per thread: the chunks c = tid + 1024 k in increasing order.  A chunk whose maximum exceeds
+// the running one raises it (rescaling the sum) and becomes the thread's best chunk; the
+// index inside that chunk is found once at the end, so the common path tracks no indices:
+// a max over the chunk, then one exp2 per element into the sum.
+template <bool BF>
 __global__ __launch_bounds__(kTokThreads) void cover_token_stats_kernel(const TokParams p) {
+  constexpr int N = BF ? 8 : 4;  // elements per 16-byte chunk
   __shared__ float sm[kTokThreads / 64], ss[kTokThreads / 64];
   __shared__ int si[kTokThreads / 64];
   const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const char* row = p.logits + (int64_t)r * p.row_stride_bytes;
-  const int per = p.bf16 ? 8 : 4;  // elements per 16-byte chunk
-  const int nfull = p.V / per;      // whole chunks; the last V % per elements come after
-  Acc acc = {-INFINITY, 0.0f, 0x7fffffff};
-  for (int c0 = tid; c0 < nfull; c0 += kTokThreads * kTokUnroll) {
+  auto chunk = [&](int c) __attribute__((always_inline)) {
+    return *(gu32x4*)((__attribute__((address_space(1))) const char*)row + (int64_t)c * 16);
+  };
+  const int nfull = p.V / N;  // whole chunks; the last V % N elements come after
+  // the placed token's logit, requested now (uniform: scalar loads, apart from the stream)
+  float xy = __builtin_nanf("");
+  if (p.logp) {
+    const int y = p.tokens[r];
+    if ((unsigned)y < (unsigned)p.V) {
+      if constexpr (BF) {
+        const uint32_t w = *(const uint32_t*)(row + ((int64_t)y * 2 & ~(int64_t)3));
+        xy = (y & 1) ? bf_hi(w) : bf_lo(w);
+      } else {
+        xy = *(const float*)(row + (int64_t)y * 4);
+      }
+    }
+  }
+  float m = -INFINITY, s = 0.0f;
+  int cbest = -1;
+  auto fold = [&](const float* x, int c) __attribute__((always_inline)) {
+    float cm = x[0];
+#pragma unroll
+    for (int e = 1; e < N; ++e) cm = __builtin_fmaxf(cm, x[e]);
+    const float mn = __builtin_fmaxf(m, cm);
+    s *= __builtin_amdgcn_exp2f((m - mn) * kLog2e);  // 1 unless the max was raised
+    cbest = cm > m ? c : cbest;
+    m = mn;
+    const float nm = -mn * kLog2e;
+    float a[N / 2];
+#pragma unroll
+    for (int e = 0; e < N / 2; ++e)
+      a[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[2 * e], kLog2e, nm)) +
+             __builtin_amdgcn_exp2f(__builtin_fmaf(x[2 * e + 1], kLog2e, nm));
+    float t = a[0];
+#pragma unroll
+    for (int e = 1; e < N / 2; ++e) t += a[e];
+    s += t;
+  };
+  // rounds in which every thread's chunks exist: no bounds tests
+  constexpr int kRound = kTokThreads * kTokUnroll;
+  int c0 = tid;
+  for (; c0 - tid + kRound <= nfull; c0 += kRound) {
+    u32x4 v[kTokUnroll];
+#pragma unroll
+    for (int u = 0; u < kTokUnroll; ++u) v[u] = chunk(c0 + u * kTokThreads);
+#pragma unroll
+    for (int u = 0; u < kTokUnroll; ++u) {
+      float x[N];
+      unpack<BF>(v[u], x);
+      fold(x, c0 + u * kTokThreads);
+    }
+  }
+  {  // the last, partial round
     u32x4 v[kTokUnroll];
 #pragma unroll
     for (int u = 0; u < kTokUnroll; ++u) {
       const int c = c0 + u * kTokThreads;
-      v[u] = c < nfull ? *(gu32x4*)((__attribute__((address_space(1))) const char*)row + (int64_t)c * 16) : (u32x4){};
+      v[u] = c < nfull ? chunk(c) : (u32x4){};
     }
 #pragma unroll
     for (int u = 0; u < kTokUnroll; ++u) {
       const int c = c0 + u * kTokThreads;
-      if (c >= nfull) break;
-      float x[8];
-      if (p.bf16) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { x[2 * e] = bf_lo(v[u][e]); x[2 * e + 1] = bf_hi(v[u][e]); }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(v[u][e]); x[e + 4] = -INFINITY; }
+      if (c < nfull) {
+        float x[N];
+        unpack<BF>(v[u], x);
+        fold(x, c);
       }
-      fold(acc, x, per, c * per);
     }
   }
+  // index of the maximum: the first element of the best chunk that holds it
+  int ibest = 0x7fffffff;
+  if (cbest >= 0) {
+    float x[N];
+    unpack<BF>(chunk(cbest), x);
+#pragma unroll
+    for (int e = N - 1; e >= 0; --e)
+      if (x[e] == m) ibest = cbest * N + e;
+  }
+  Acc acc = {m, s, ibest};
   // the tail: one element per thread, read at its own width (never past the row's end)
-  if (tid < p.V - nfull * per) {
-    const int j = nfull * per + tid;
-    float x[8];
-    x[0] = p.bf16 ? __uint_as_float((uint32_t)(*(const uint16_t*)(row + (int64_t)j * 2)) << 16)
-                  : *(const float*)(row + (int64_t)j * 4);
-    fold(acc, x, 1, j);
+  if (tid < p.V - nfull * N) {
+    const int j = nfull * N + tid;
+    const float xj = BF ? __uint_as_float((uint32_t)(*(const uint16_t*)(row + (int64_t)j * 2)) << 16)
+                        : *(const float*)(row + (int64_t)j * 4);
+    acc = merge(acc, Acc{xj, 1.0f, j});
   }
   // wave, then workgroup
 #pragma unroll
@@ -138,24 +190,22 @@ __global__ __launch_bounds__(kTokThreads) void cover_token_stats_kernel(const To
   }
   if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; si[wave] = acc.i; }
   __syncthreads();
-  if (tid == 0) {
-    Acc t = {sm[0], ss[0], si[0]};
-    for (int w = 1; w < kTokThreads / 64; ++w) t = merge(t, Acc{sm[w], ss[w], si[w]});
-    const float lz = t.m + __builtin_amdgcn_logf(t.s) * kLn2;  // natural log-sum-exp
-    if (p.conf) p.conf[r] = 1.0f / t.s;                         // exp(max - lz)
-    if (p.argmax) p.argmax[r] = t.i;
-    if (p.logp) {
-      const int y = p.tokens[r];
-      float xy = __builtin_nanf("");
-      if ((unsigned)y < (unsigned)p.V) {
-        if (p.bf16) {
-          const uint16_t h = *(const uint16_t*)(row + (int64_t)y * 2);
-          xy = __uint_as_float((uint32_t)h << 16);
-        } else {
-          xy = *(const float*)(row + (int64_t)y * 4);
-        }
-      }
-      p.logp[r] = xy - lz;
+  if (wave == 0) {  // the 16 wave results: a tree over lanes 0..15 of wave 0
+    constexpr int W = kTokThreads / 64;
+    Acc t = lane < W ? Acc{sm[lane], ss[lane], si[lane]} : Acc{-INFINITY, 0.0f, 0x7fffffff};
+#pragma unroll
+    for (int off = W / 2; off >= 1; off >>= 1) {
+      Acc o;
+      o.m = __shfl_xor(t.m, off);
+      o.s = __shfl_xor(t.s, off);
+      o.i = __shfl_xor(t.i, off);
+      t = merge(t, o);
+    }
+    if (lane == 0) {
+      const float lz = t.m + __builtin_amdgcn_logf(t.s) * kLn2;  // natural log-sum-exp
+      if (p.conf) p.conf[r] = 1.0f / t.s;                         // exp(max - lz)
+      if (p.argmax) p.argmax[r] = t.i;
+      if (p.logp) p.logp[r] = xy - lz;
     }
   }
 }
@@ -352,8 +402,10 @@ hipError_t launch_token_stats(const TokenArgs& a, hipStream_t stream) {
   p.argmax = a.argmax;
   p.row_stride_bytes = a.row_stride * (a.bf16 ? 2 : 4);
   p.V = a.V;
-  p.bf16 = a.bf16;
-  hipLaunchKernelGGL(cover_token_stats_kernel, dim3((unsigned)a.R), dim3(kTokThreads), 0, stream, p);
+  if (a.bf16)
+    hipLaunchKernelGGL(cover_token_stats_kernel<true>, dim3((unsigned)a.R), dim3(kTokThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cover_token_stats_kernel<false>, dim3((unsigned)a.R), dim3(kTokThreads), 0, stream, p);
   return hipGetLastError();
 }
 
