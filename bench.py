@@ -655,8 +655,8 @@ def bench_block(args, dev, stream) -> int:
     """cover_attn_rect at the LLaDA-8B layer shape (B=1, 32 heads of 128, L=1024): the
     generated block of 256 rows and prefix-cache block sizes of 64 and 32 rows against all
     1024 keys (Sec. 6.6), inputs resident.  Prints one JSON line per block size with the
-    launch time (both kernels, HIP events over back-to-back launches) and the roofline of an
-    HBM-bound call: algorithmic bytes = K and V of all keys (seed rows from the cache) + the
+    launch time (one launch, or the split and merge kernels for n_split > 1; HIP events over
+    back-to-back calls) and the roofline of an HBM-bound call: algorithmic bytes = K and V of all keys (seed rows from the cache) + the
     block's q and out + lse."""
     import torch
     from paper_2602_06161_amd import cover, synth
@@ -668,11 +668,10 @@ def bench_block(args, dev, stream) -> int:
     K = max(1, args.steps)
     for Lq, q_off in ((256, 768), (64, 896), (32, 992)):
         qb = q[:, :, q_off:q_off + Lq].contiguous()
-        n = cover.rect_splits(B, H, Lq, L)
-        ws = torch.empty(cover.rect_workspace(B, H, Lq, n), device=dev, dtype=torch.float32)
-        out, lse = torch.empty_like(qb), torch.empty((B, H, Lq), device=dev, dtype=torch.float32)
-        call = lambda: cover.cover_attn_rect(qb, kl, vl, kc, vc, q_off, si, ns, out=out, lse=lse,
-                                             n_split=n, workspace=ws, stream=stream)
+        # arguments marshalled once: a call is one C-ABI call, so the loop is not bound by
+        # Python's per-call overhead (about 12 us, near the kernel's own time)
+        call = cover.PreparedRect(qb, kl, vl, kc, vc, q_off, si, ns, stream=stream)
+        n = call.n_split
         for _ in range(max(1, args.warmup)):
             call()
         torch.cuda.synchronize()
@@ -684,7 +683,7 @@ def bench_block(args, dev, stream) -> int:
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / K
         alg = B * H * L * d * 2 * 2 + 2 * B * H * Lq * d * 2 + B * H * Lq * 4
-        rec = 2 * B * H * n * Lq * cover.COVER_RECT_RECORD * 4
+        rec = 2 * cover.rect_workspace(B, H, Lq, n) * 4
         flops = 4 * B * H * Lq * L * d
         gbs = alg / us / 1e3
         print(json.dumps({

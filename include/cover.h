@@ -290,8 +290,11 @@ cover_status cover_attn_stats_noalloc(const void* q, const void* k_live, const v
  * and stride rules, with attn.L the number of keys; q and out hold Lq rows at the q strides)
  * plus the query block [q_off, q_off + Lq) and the number of key splits.
  *   q_off, Lq   0 <= q_off, 0 <= Lq, q_off + Lq <= attn.L (Lq == 0 is a no-op)
- *   n_split     1 <= n_split <= 256: the keys are cut into n_split ranges processed in
- *               parallel and merged (more splits fill the GPU when Lq is small)
+ *   n_split     1 <= n_split <= 256.  1: one launch, one workgroup per 32 query rows whose
+ *               waves split the keys among themselves (no workspace).  > 1: the keys are cut
+ *               into n_split ranges processed by separate workgroups and merged by a second
+ *               launch (more workgroups per query row; the partial results go through the
+ *               workspace)
  */
 typedef struct {
   cover_attn_desc attn;
@@ -301,9 +304,9 @@ typedef struct {
 
 /* 4-byte words per (row, split) record of the cover_attn_rect workspace. */
 #define COVER_RECT_RECORD 68
-/* Workspace of cover_attn_rect in floats. */
+/* Workspace of cover_attn_rect in floats (none for n_split == 1). */
 #define COVER_ATTN_RECT_WORKSPACE(B, Hq, Lq, n_split) \
-  ((int64_t)(B) * (Hq) * (n_split) * (Lq) * COVER_RECT_RECORD)
+  ((n_split) > 1 ? (int64_t)(B) * (Hq) * (n_split) * (Lq) * COVER_RECT_RECORD : (int64_t)0)
 
 /*
  * cover_attn_rect -- COVER attention for one block of query rows against all L keys (the
@@ -315,11 +318,13 @@ typedef struct {
  * the leave-one-out diagonal of a seed row, App. B): q holds only the block's Lq rows.
  * Seeds may lie anywhere in [0, L), inside the block or not.
  * Arguments as for cover_attn_fwd; out [B,Hq,Lq,d] at the q strides; lse fp32 [B,Hq,Lq]
- * contiguous (may be NULL); workspace: device fp32 buffer of
+ * contiguous (may be NULL); workspace: for n_split > 1 a device fp32 buffer of
  * COVER_ATTN_RECT_WORKSPACE(B, Hq, Lq, n_split) floats owned by the caller (contents on
- * entry ignored, on exit unspecified).  Two kernel launches on `stream` (partial results
- * per key split, then a merge in a fixed order: deterministic).
- * Returns COVER_ERR_UNSUPPORTED for a dtype other than bf16, d != 128 or L > COVER_MAX_L.
+ * entry ignored, on exit unspecified); for n_split == 1 not used (may be NULL).  One kernel
+ * launch on `stream` for n_split == 1, two otherwise (partial results per key split, then
+ * a merge); every sum runs in a fixed order, so results are deterministic.
+ * Returns COVER_ERR_UNSUPPORTED for a dtype other than bf16, d != 128, L > COVER_MAX_L, or
+ * n_split == 1 with kv_sl >= 2^26.
  */
 cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_live,
                              const void* k_cache, const void* v_cache,

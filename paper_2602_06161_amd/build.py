@@ -45,7 +45,7 @@ SOURCES = {
 
 
 # sources compiled a second time, with these flags, for LIB_TIMING
-TIMING = {"cover_attn_w4.hip": ["-DCOVER_ATTN_TIMING=1"]}
+TIMING = {"cover_attn_w4.hip": ["-DCOVER_ATTN_TIMING=1"], "cover_attn_rect.hip": ["-DCOVER_RECT_TIMING=1"]}
 # sources of LIB_TIMING only (the MFMA-counter calibration kernel)
 TIMING_ONLY = {"cover_calib.hip": []}
 

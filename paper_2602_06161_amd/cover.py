@@ -203,13 +203,19 @@ def cover_attn_fwd(q, k_live, v_live, k_cache, v_cache, seed_idx=None, n_seed=No
 
 
 def rect_workspace(B: int, Hq: int, Lq: int, n_split: int) -> int:
-    """Floats of workspace cover_attn_rect needs (COVER_ATTN_RECT_WORKSPACE)."""
-    return B * Hq * n_split * Lq * COVER_RECT_RECORD
+    """Floats of workspace cover_attn_rect needs (COVER_ATTN_RECT_WORKSPACE): none for the
+    single launch (n_split == 1)."""
+    return B * Hq * n_split * Lq * COVER_RECT_RECORD if n_split > 1 else 0
 
 
 def rect_splits(B: int, Hq: int, Lq: int, L: int) -> int:
-    """Key splits: about 256 workgroups in all (one per compute unit; the split kernel is
-    bound by each workgroup's serial work, not by HBM), with at least 128 keys per split."""
+    """Key splits.  1 (the single launch: one workgroup per 32 query rows, its waves split the
+    keys) unless the sequence is long and the block leaves most CUs idle: that kernel reads
+    all of a head's K and V through one CU per 32 rows, about 100 GB/s per CU, so past 2048
+    keys with fewer than 256 workgroups the keys are split across workgroups instead (about
+    256 workgroups of at least 128 keys each, merged by a second launch)."""
+    if L <= 2048 or B * Hq * ((Lq + 31) // 32) >= 256:
+        return 1
     wgs = B * Hq * ((Lq + 127) // 128)
     n = min(-(-256 // wgs), -(-L // 128))
     return max(1, min(n, 256))
@@ -241,9 +247,12 @@ def cover_attn_rect(q, k_live, v_live, k_cache, v_cache, q_off: int, seed_idx=No
     if n_split is None:
         n_split = rect_splits(B, Hq, Lq, L)
     need = rect_workspace(B, Hq, Lq, n_split)
-    if workspace is None:
-        workspace = torch.empty(max(need, 4), device=q.device, dtype=torch.float32)
-    if workspace.dtype != torch.float32 or workspace.numel() < need or not workspace.is_contiguous():
+    if need == 0:
+        workspace = None  # not used by the single launch
+    elif workspace is None:
+        workspace = torch.empty(need, device=q.device, dtype=torch.float32)
+    if workspace is not None and (workspace.dtype != torch.float32 or workspace.numel() < need
+                                  or not workspace.is_contiguous()):
         raise ValueError(f"workspace must be contiguous fp32 with at least {need} elements")
     ad = attn_desc(q, k_live, max_seeds, scale)
     ad.L = L
@@ -471,6 +480,40 @@ class PreparedAttn:
         st = self._fn(*self._args)
         if st != COVER_OK:
             raise CoverError(st, "cover_attn_fwd")
+
+
+class PreparedRect:
+    """A cover_attn_rect call with its arguments marshalled once (see PreparedAttn)."""
+
+    def __init__(self, q, k_live, v_live, k_cache, v_cache, q_off: int, seed_idx=None,
+                 n_seed=None, out=None, lse=None, scale: float = 0.0, n_split=None, workspace=None,
+                 stream=None):
+        B, Hq, Lq, d = q.shape
+        L = k_live.shape[2]
+        if n_split is None:
+            n_split = rect_splits(B, Hq, Lq, L)
+        need = rect_workspace(B, Hq, Lq, n_split)
+        if need and workspace is None:
+            workspace = torch.empty(need, device=q.device, dtype=torch.float32)
+        self.out, self.lse = cover_attn_rect(q, k_live, v_live, k_cache, v_cache, q_off, seed_idx,
+                                             n_seed, out=out, lse=lse, scale=scale, n_split=n_split,
+                                             workspace=workspace, stream=stream)
+        self.n_split = n_split
+        ws = workspace if need else None
+        self._keep = (q, k_live, v_live, k_cache, v_cache, seed_idx, n_seed, self.out, self.lse, ws)
+        max_seeds = 0 if seed_idx is None else seed_idx.shape[-1]
+        ad = attn_desc(q, k_live, max_seeds, scale)
+        ad.L = L
+        self._desc = RectDesc(ad, q_off, Lq, n_split)
+        self._args = (_ptr(q), _ptr(k_live), _ptr(v_live), _ptr(k_cache), _ptr(v_cache),
+                      _ptr(seed_idx), _ptr(n_seed), _ptr(self.out), _ptr(self.lse), _ptr(ws),
+                      ctypes.byref(self._desc), _stream(stream))
+        self._fn = lib().cover_attn_rect
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != COVER_OK:
+            raise CoverError(st, "cover_attn_rect")
 
 
 class PreparedSelect:

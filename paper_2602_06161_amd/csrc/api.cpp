@@ -288,13 +288,20 @@ cover_status cover_attn_rect(const void* q, const void* k_live, const void* v_li
   if (D.max_seeds > 0 && (!seed_idx || !n_seed || !aligned(seed_idx, 4) || !aligned(n_seed, 4)))
     return COVER_ERR_INVALID;
   if (lse && !aligned(lse, 4)) return COVER_ERR_INVALID;
-  if (!workspace || !aligned(workspace, 16)) return COVER_ERR_INVALID;
-  if ((int64_t)D.B * D.Hq * ((Lq + 127) / 128) * n_split > 0x7fffffffLL) return COVER_ERR_UNSUPPORTED;
+  if (n_split > 1 && (!workspace || !aligned(workspace, 16))) return COVER_ERR_INVALID;
+  if (n_split == 1 && D.kv_sl >= (int64_t(1) << 26)) return COVER_ERR_UNSUPPORTED;
+  // grids: at most 2^32 work-items per launch (512 per workgroup for n_split == 1; 256 for the
+  // split kernel, and one 64-lane wave per row for the merge)
+  if (n_split == 1 && (int64_t)D.B * D.Hq * ((Lq + 31) / 32) > (int64_t(1) << 23) - 8)
+    return COVER_ERR_UNSUPPORTED;
+  if (n_split > 1 && ((int64_t)D.B * D.Hq * ((Lq + 127) / 128) * n_split > (int64_t(1) << 24) - 1 ||
+                      (int64_t)D.B * D.Hq * Lq > (int64_t(1) << 26) - 4))
+    return COVER_ERR_UNSUPPORTED;
   cover::RectArgs a;
   a.q = q; a.k_live = k_live; a.v_live = v_live; a.k_cache = k_cache; a.v_cache = v_cache;
   a.seed_idx = D.max_seeds > 0 ? seed_idx : nullptr;
   a.n_seed = D.max_seeds > 0 ? n_seed : nullptr;
-  a.out = out; a.lse = lse; a.workspace = workspace;
+  a.out = out; a.lse = lse; a.workspace = n_split > 1 ? workspace : nullptr;
   a.B = D.B; a.Hq = D.Hq; a.Hkv = D.Hkv; a.L = D.L; a.max_seeds = D.max_seeds;
   a.q_off = q_off; a.Lq = Lq; a.n_split = n_split;
   a.scale = D.scale > 0.0f ? D.scale : 1.0f / sqrtf((float)D.d);

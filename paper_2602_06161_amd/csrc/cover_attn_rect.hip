@@ -36,8 +36,10 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) char lds_t;
+typedef __attribute__((address_space(1))) const char gmem_t;
 
 constexpr int kD = 128;
 constexpr int kRow = 2 * kD;            // bytes per K/V row
@@ -61,6 +63,7 @@ struct RectParams {
   __bf16* out;
   float* lse;
   int B, Hq, Hkv, L, Lq, q_off, max_seeds, group, n_qt, n_split, split_stages;
+  int n_wg, xcd_slots;  // single-launch form: workgroups, logical tiles per XCD
   float c2;  // scale * log2(e)
   int64_t q_sb, q_sh, q_sl, kv_sb, kv_sh, kv_sl;
 };
@@ -383,7 +386,428 @@ __global__ __launch_bounds__(256) void cover_attn_rect_merge_kernel(const RectPa
   if (p.lse && lane == 0) p.lse[row] = (M + __builtin_amdgcn_logf(den)) * kLn2;
 }
 
+
+// ---------------------------------------------------------------------------------------
+// Single-launch form (n_split == 1): one workgroup of 8 waves per (batch, query head,
+// 32-query tile).  A CU's load path, not HBM, bounds a short block (about 100 GB/s per CU),
+// and the merge of key splits held by different workgroups costs a second launch; so the
+// key split stays inside the workgroup: wave w takes the w-th eighth of the 32-key stages
+// and streams them through a K slot and a V slot of its own by global-to-LDS loads (no
+// barrier in the loop), each slot refilled as soon as it has been read.  The eight partial
+// (max, sum, O) states and a seed row's live diagonal term are merged through LDS at the end.
+// Workgroups that share a KV head are placed on one XCD, so its L2 serves their re-reads.
+// ---------------------------------------------------------------------------------------
+constexpr int kTW = 8;             // waves per workgroup
+constexpr int kTQ = 32;            // queries per workgroup
+constexpr int kSB = kStage * kRow; // bytes of one stage of K (or V)
+constexpr int kTSeeds = 64 * kTW;  // seed positions fetched into LDS (the rest: plain loads)
+constexpr float kLazyT = 8.0f;
+
+// s_waitcnt immediate that waits for vmcnt <= n only
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xf00; }
+
+// Global -> LDS loads: lane l's 16 bytes (4 for the dword form) land at LDS byte lds + 16 l
+// (+ 4 l); lds is wave-uniform.  The compiler does not track them: every read of their data
+// follows an explicit vmcnt wait of the issuing wave.  A wave's loads land in issue order.
+__device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_t*)ptr);
+}
+__device__ __forceinline__ void dma16(uint32_t lds, gmem_t* addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(lds), "v"((uint64_t)addr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma16s(uint32_t lds, gmem_t* base, uint32_t voff) {  // uniform base
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(lds), "v"(voff), "s"(base) : "memory", "m0");
+}
+// the uniform-base load for the lanes of `mask` only (exec set and restored inside the
+// statement; the scalar moves and the nop keep the load behind any VALU write of its operands)
+__device__ __forceinline__ void dma16m(uint32_t lds, gmem_t* base, uint32_t voff, uint64_t mask) {
+  uint64_t save;
+  asm volatile("s_mov_b64 %0, exec\n\ts_mov_b64 exec, %1\n\ts_mov_b32 m0, %2\n\ts_nop 1\n\t"
+               "global_load_lds_dwordx4 %3, %4\n\ts_mov_b64 exec, %0"
+               : "=&s"(save) : "s"(mask), "s"(lds), "v"(voff), "s"(base) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(uint32_t lds, gmem_t* addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+               :: "s"(lds), "v"((uint64_t)addr) : "memory", "m0");
+}
+// lanes 16 k .. 16 k + 15 for each set bit k of a 4-bit value
+__device__ __forceinline__ uint64_t lane_quads(uint32_t n) {
+  const uint64_t m = (uint64_t)(n & 1u) | ((uint64_t)(n & 2u) << 15) | ((uint64_t)(n & 4u) << 30) |
+                     ((uint64_t)(n & 8u) << 45);
+  return (m << 16) - m;
+}
+__device__ __forceinline__ gmem_t* uniform_ptr(const void* ptr) {
+  const uint64_t v = (uint64_t)ptr;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (gmem_t*)(((uint64_t)hi << 32) | lo);
+}
+
+// Phase timing (a separate build of the library, -DCOVER_RECT_TIMING=1, used only to measure
+// where a workgroup's time goes): lane 0 of every wave of the first kTimeWG logical
+// workgroups stores the shader-clock counter at fixed points.  Slots: 0 start, 1 seed list
+// and Q landed, 2 seed bitmap built, 3 first stage landed, 4 + i top of the wave's stage i
+// (i < 16), 20 loop done, 21 partial states in LDS (after the barrier), 22 end.
+#ifndef COVER_RECT_TIMING
+#define COVER_RECT_TIMING 0
+#endif
+#if COVER_RECT_TIMING
+constexpr int kTimeWG = 1024, kTimeSlots = 32;
+__device__ uint64_t g_rect_times[kTimeWG * kTW * kTimeSlots];
+#define RECT_TSTAMP(slot)                                                                        \
+  do {                                                                                           \
+    if (li < kTimeWG && lane == 0)                                                               \
+      g_rect_times[((int64_t)li * kTW + wave) * kTimeSlots + (slot)] = __builtin_readcyclecounter(); \
+  } while (0)
+#else
+#define RECT_TSTAMP(slot) do {} while (0)
+#endif
+
+__global__ __launch_bounds__(64 * kTW, 1) void cover_attn_tile_kernel(const RectParams p) {
+  // per wave: a K slot and a V slot (at the end: its partial O, 32 rows of 128 fp32);
+  // the tile's Q; the seed bitmap of the sequence; the seed list; the partial maxima and sums
+  __shared__ __attribute__((aligned(1024))) char sKV[kTW][2][kSB];
+  __shared__ __attribute__((aligned(1024))) char sQ[kTQ * kRow];
+  __shared__ uint32_t bits[kMaxWords];
+  __shared__ __attribute__((aligned(16))) int32_t sSeeds[kTSeeds];
+  __shared__ __attribute__((aligned(16))) int32_t sNs[4];
+  __shared__ float sM[kTW][kTQ], sL[kTW][kTQ];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hl = lane >> 5;
+
+  // workgroup -> (b, h, tile); consecutive logical tiles (those of one KV head) share an XCD
+  const int li = (blockIdx.x & 7) * p.xcd_slots + (blockIdx.x >> 3);
+  if (li >= p.n_wg) return;
+  RECT_TSTAMP(0);
+  const int qt = li % p.n_qt, bh = li / p.n_qt;
+  const int h = bh % p.Hq, b = bh / p.Hq, g = h / p.group;
+  const int L = p.L;
+  const int nst = (L + kStage - 1) / kStage;
+  const int s0 = wave * nst / kTW, s1 = (wave + 1) * nst / kTW;  // this wave's stages
+  const int ragged = L % kStage ? nst - 1 : -1;
+  const int nW = (L + 31) >> 5;
+  for (int w = tid; w < nW; w += 64 * kTW) bits[w] = 0u;
+
+  // load geometry: load j of a stage covers stage rows 4 j + lane / 16 at physical chunk
+  // lane % 16, i.e. LDS byte 1024 j + 16 lane of the slot; the source chunk is the one the
+  // slot's swizzle puts there (K: chunk ^ row % 16; V: chunk ^ 4 (row % 4))
+  const int64_t row_bytes = p.kv_sl * 2, stage_bytes = kStage * row_bytes;
+  uint32_t offK[8], offV[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = 4 * j + (lane >> 4), pc = lane & 15;
+    offK[j] = (uint32_t)(row * row_bytes) + ((pc ^ (row & 15)) << 4);
+    offV[j] = (uint32_t)(row * row_bytes) + ((pc ^ ((row & 3) << 2)) << 4);
+  }
+  const int64_t kvoff = b * p.kv_sb + g * p.kv_sh;
+  const char* const klc = (const char*)(p.kl + kvoff);
+  const char* const kcc = (const char*)(p.kc + kvoff);
+  const char* const vlc = (const char*)(p.vl + kvoff);
+  const char* const vcc = (const char*)(p.vc + kvoff);
+  const uint32_t slotK = lds_addr(sKV[wave][0]), slotV = lds_addr(sKV[wave][1]);
+  // one stage: every row from the live tensor, or (with seeds = the stage's seed word) a seed
+  // row from the cache; rows past L clamped into the sequence
+  auto ld_stage = [&](uint32_t slot, const char* live, const char* cache, const uint32_t* off, int st,
+                      uint32_t seeds) __attribute__((always_inline)) {
+    if (st == ragged || seeds != 0u) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int row = 4 * j + (lane >> 4);
+        const int key = min(st * kStage + row, L - 1);
+        const char* src = ((seeds >> row) & 1u) ? cache : live;
+        dma16(slot + 1024 * j, (gmem_t*)(src + key * row_bytes + (off[j] - (uint32_t)(row * row_bytes))));
+      }
+    } else {
+      gmem_t* base = uniform_ptr(live + st * stage_bytes);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dma16s(slot + 1024 * j, base, off[j]);
+    }
+  };
+  auto seed_word = [&](int st) __attribute__((always_inline)) -> uint32_t {
+    return __builtin_amdgcn_readfirstlane(bits[st]);
+  };
+  // the seed rows of the first stage again (its loads went out before the seeds were known),
+  // from the cache, issued after the live loads of the same slot so that they land last; a
+  // load with no seed row among its four is skipped
+  auto patch = [&](uint32_t slot, const char* cache, const uint32_t* off, int st)
+                   __attribute__((always_inline)) {
+    const uint32_t w = seed_word(st);
+    if (w == 0u) return;
+    gmem_t* base = uniform_ptr(cache + st * stage_bytes);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t nib = (w >> (4 * j)) & 15u;
+      if (nib) dma16m(slot + 1024 * j, base, off[j], lane_quads(nib));
+    }
+  };
+
+  // ---- prologue: the seed list, Q, and this wave's first stage from the live tensors ------
+  const int64_t sbase = (int64_t)b * p.max_seeds;
+  if (p.max_seeds > 0) {
+    if (tid == 0) dma4(lds_addr(sNs), (gmem_t*)(p.n_seed + b));
+    const int e = 64 * wave + lane;
+    if (e < p.max_seeds) dma4(lds_addr((const char*)sSeeds + 256 * wave), (gmem_t*)(p.seed_idx + sbase + e));
+  }
+  const __bf16* qbase = p.q + b * p.q_sb + h * p.q_sh;
+  {
+    const int row = 4 * wave + (lane >> 4), pc = lane & 15;
+    const int qi = min(qt * kTQ + row, p.Lq - 1);
+    dma16(lds_addr(sQ + 1024 * wave), (gmem_t*)((const char*)(qbase + (int64_t)qi * p.q_sl) + ((pc ^ (row & 15)) << 4)));
+  }
+  if (s0 < s1) {
+    ld_stage(slotK, klc, kcc, offK, s0, 0u);
+    ld_stage(slotV, vlc, vcc, offV, s0, 0u);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(16));  // the seed list and Q have landed
+  } else {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  }
+  RECT_TSTAMP(1);
+  __syncthreads();
+  if (p.max_seeds > 0) {
+    int ns = sNs[0];
+    ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
+    if (tid < ns && tid < kTSeeds) {
+      const int j = sSeeds[tid];
+      if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
+    }
+    for (int t = tid + kTSeeds; t < ns; t += 64 * kTW) {  // long seed lists
+      const int j = p.seed_idx[sbase + t];
+      if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
+    }
+  }
+  __syncthreads();
+  RECT_TSTAMP(2);
+  auto is_seed = [&](int j) __attribute__((always_inline)) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
+  if (s0 < s1) {
+    patch(slotK, kcc, offK, s0);
+    patch(slotV, vcc, offV, s0);
+  }
+
+  // Q fragments (B operand of S^T = K Q^T): query l32, d-chunk 2 ks + hl
+  bf16x8 qreg[kD / 16];
+#pragma unroll
+  for (int ks = 0; ks < kD / 16; ++ks)
+    qreg[ks] = *(const __attribute__((address_space(3))) bf16x8*)((const lds_t*)sQ + k_off(l32, 2 * ks + hl));
+  const int qrow = min(qt * kTQ + l32, p.Lq - 1);
+  const int pos = p.q_off + qrow;
+  const bool row_seed = is_seed(pos);
+
+  // the live key and value rows of the seed rows this wave finishes: lane group fq = lane / 16
+  // takes query kFin wave + fq, dims 8 (lane % 16) .. + 7, requested now and used in the merge
+  constexpr int kFin = kTQ / kTW;
+  const int fq = lane >> 4, fj = lane & 15;
+  const int qfin = qt * kTQ + kFin * wave + fq;
+  const bool fin_ok = qfin < p.Lq;
+  const bool fseed = fin_ok && is_seed(p.q_off + qfin);
+  u32x4 kd = {0u, 0u, 0u, 0u}, vd = {0u, 0u, 0u, 0u};
+  if (fseed) {
+    const int64_t ro = kvoff + (int64_t)(p.q_off + qfin) * p.kv_sl + 8 * fj;
+    kd = *(const u32x4*)(p.kl + ro);
+    vd = *(const u32x4*)(p.vl + ro);
+  }
+
+  // V^T operand addresses (as in the split kernel)
+  uint32_t vaddr[kD / 32];
+  {
+    const int G = lane >> 4, ii = lane & 15;
+    const int row = 4 * (G >> 1) + (ii >> 2);
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db) vaddr[db] = v_elem(row, db * 32 + 16 * (G & 1) + 4 * (ii & 3));
+  }
+  f32x16 o[kD / 32];
+#pragma unroll
+  for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+  float m = kInit, l = 0.0f;
+  const lds_t* const kb = (const lds_t*)sKV[wave][0];
+  const lds_t* const vb = (const lds_t*)sKV[wave][1];
+
+  for (int st = s0; st < s1; ++st) {
+    const bool more = st + 1 < s1;
+    // K(st) has landed: younger are V(st)'s 8 loads; at the first stage everything is waited
+    // for (the patches of the prologue are counted nowhere)
+    if (st == s0) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));
+    if (st == s0) RECT_TSTAMP(3);
+    if (st - s0 < 16) RECT_TSTAMP(4 + st - s0);
+    bf16x8 ka[kD / 16];
+#pragma unroll
+    for (int ks = 0; ks < kD / 16; ++ks)
+      ka[ks] = *(const __attribute__((address_space(3))) bf16x8*)(kb + k_off(l32, 2 * ks + hl));
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the K slot is read: refill it
+    if (more) ld_stage(slotK, klc, kcc, offK, st + 1, seed_word(st + 1));
+    f32x16 sc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < kD / 16; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], sc, 0, 0, 0);
+    // register r holds key k0 + 8 (r / 4) + 4 hl + r % 4 of query qrow
+    const int k0 = st * kStage;
+    const bool edge = k0 + kStage > L;
+    const bool diag = row_seed && pos >= k0 && pos < k0 + kStage;
+    float mx = kInit;
+    if (__builtin_amdgcn_ballot_w64(diag) != 0 || edge) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        float t = sc[r] * p.c2;
+        if (key >= L || (diag && key == pos)) t = -INFINITY;
+        sc[r] = t;
+        mx = __builtin_fmaxf(mx, t);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sc[r] *= p.c2;
+        mx = __builtin_fmaxf(mx, sc[r]);
+      }
+    }
+    mx = pair_max(mx);
+    if (st == s0) {
+      m = mx;
+    } else if (__builtin_amdgcn_ballot_w64(mx > m + kLazyT)) {
+      const float mn = __builtin_fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);
+      l *= alpha;
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) o[db] *= alpha;
+      m = mn;
+    }
+    bf16x8 pk[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float pr = __builtin_amdgcn_exp2f(sc[8 * kk + e] - m);
+        l += pr;
+        pk[kk][e] = (__bf16)pr;
+      }
+    // V(st) has landed: younger are K(st + 1)'s 8 loads, if there is a stage st + 1
+    if (more) __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    bf16x8 va[2][kD / 32];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db) {
+        const lds_t* base = vb + vaddr[db] + kk * 16 * kRow;
+        va[kk][db] = __builtin_bit_cast(
+            bf16x8, __builtin_shufflevector(v_tr(base), v_tr(base + 8 * kRow), 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the V slot is read: refill it
+    if (more) {
+      ld_stage(slotV, vlc, vcc, offV, st + 1, seed_word(st + 1));
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int db = 0; db < kD / 32; ++db)
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kk][db], pk[kk], o[db], 0, 0, 0);
+  }
+
+  // ---- merge: every wave's (max, sum, O) through LDS ---------------------------------------
+  // O goes to this wave's own slots (its loads have all landed and been read): row l32, 16-byte
+  // chunk c (dims 4 c .. 4 c + 3) at byte 512 l32 + 16 (c ^ l32)
+  RECT_TSTAMP(20);
+  const float lt = pair_sum(l);
+  if (hl == 0) {
+    sM[wave][l32] = m;
+    sL[wave][l32] = lt;
+  }
+  {
+    lds_t* const ob = (lds_t*)sKV[wave][0] + 512 * l32;
+#pragma unroll
+    for (int db = 0; db < kD / 32; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int c = 8 * db + 2 * gq + hl;
+        *(__attribute__((address_space(3))) f32x4*)(ob + ((c ^ l32) << 4)) =
+            f32x4{o[db][4 * gq], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]};
+      }
+  }
+  __syncthreads();
+  RECT_TSTAMP(21);
+  // wave w finishes queries kFin w + fq (lane group fq), lane dims 8 fj .. 8 fj + 7; every
+  // LDS read of the merge is requested before the first is used
+  {
+    const int f = kFin * wave + fq;
+    float mw[kTW], lw[kTW];
+    f32x4 ow[kTW][2];
+#pragma unroll
+    for (int w = 0; w < kTW; ++w) {
+      mw[w] = sM[w][f];
+      lw[w] = sL[w][f];
+      const lds_t* rb = (const lds_t*)sKV[w][0] + 512 * f;
+      ow[w][0] = *(const __attribute__((address_space(3))) f32x4*)(rb + (((2 * fj) ^ f) << 4));
+      ow[w][1] = *(const __attribute__((address_space(3))) f32x4*)(rb + (((2 * fj + 1) ^ f) << 4));
+    }
+    const u32x4 qv = *(const __attribute__((address_space(3))) u32x4*)((const lds_t*)sQ + k_off(f, fj));
+    float M = kInit;
+#pragma unroll
+    for (int w = 0; w < kTW; ++w) M = __builtin_fmaxf(M, mw[w]);
+    // the live diagonal score q . k_live(pos) of a seed row (App. B.4), summed over the
+    // group's 16 lanes
+    float dot = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      dot = __builtin_fmaf(__uint_as_float(qv[e] << 16), __uint_as_float(kd[e] << 16), dot);
+      dot = __builtin_fmaf(__uint_as_float(qv[e] & 0xffff0000u), __uint_as_float(kd[e] & 0xffff0000u), dot);
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) dot += __shfl_xor(dot, off);
+    const float t = dot * p.c2;
+    if (fseed) M = __builtin_fmaxf(M, t);
+    float den = 0.0f, acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kTW; ++w) {
+      const float a = __builtin_amdgcn_exp2f(mw[w] - M);
+      den = __builtin_fmaf(lw[w], a, den);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[e] = __builtin_fmaf(a, ow[w][0][e], acc[e]);
+        acc[4 + e] = __builtin_fmaf(a, ow[w][1][e], acc[4 + e]);
+      }
+    }
+    if (fseed) {
+      const float pd = __builtin_amdgcn_exp2f(t - M);
+      den += pd;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = __builtin_fmaf(pd, __uint_as_float(vd[e] << 16), acc[2 * e]);
+        acc[2 * e + 1] = __builtin_fmaf(pd, __uint_as_float(vd[e] & 0xffff0000u), acc[2 * e + 1]);
+      }
+    }
+    if (fin_ok) {
+      const float inv = 1.0f / den;
+      bf16x8 ob;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ob[e] = (__bf16)(acc[e] * inv);
+      *(bf16x8*)(p.out + b * p.q_sb + h * p.q_sh + (int64_t)qfin * p.q_sl + 8 * fj) = ob;
+      if (p.lse && fj == 0) p.lse[(int64_t)bh * p.Lq + qfin] = (M + __builtin_amdgcn_logf(den)) * kLn2;
+    }
+  }
+  RECT_TSTAMP(22);
+}
+
 }  // namespace
+
+#if COVER_RECT_TIMING
+// Copies the timing slots of the last launch of the single-launch kernel (layout
+// [workgroup][wave][slot], 1024 x 8 x 32 values) to host memory; waits for the device.  Only
+// in the timing build of the library.
+extern "C" int cover_rect_timing_read(uint64_t* host, int64_t n) {
+  const int64_t cap = (int64_t)kTimeWG * kTW * kTimeSlots;
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(g_rect_times), sizeof(uint64_t) * (n < cap ? n : cap),
+                                  0, hipMemcpyDeviceToHost);
+}
+#endif
 
 hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream) {
   RectParams p;
@@ -400,6 +824,15 @@ hipError_t launch_attn_rect(const RectArgs& a, hipStream_t stream) {
   p.c2 = a.scale * 1.44269504088896341f;
   p.q_sb = a.q_sb; p.q_sh = a.q_sh; p.q_sl = a.q_sl;
   p.kv_sb = a.kv_sb; p.kv_sh = a.kv_sh; p.kv_sl = a.kv_sl;
+  if (a.n_split == 1) {  // single launch, no workspace (kv_sl < 2^26: 32-bit in-stage offsets)
+    p.n_qt = (a.Lq + kTQ - 1) / kTQ;
+    const int64_t n = (int64_t)a.B * a.Hq * p.n_qt;
+    p.n_wg = (int)n;
+    p.xcd_slots = (int)((n + 7) / 8);
+    hipLaunchKernelGGL(cover_attn_tile_kernel, dim3((unsigned)(8 * (int64_t)p.xcd_slots)), dim3(64 * kTW), 0,
+                       stream, p);
+    return hipGetLastError();
+  }
   const int64_t nwg = (int64_t)a.B * a.Hq * p.n_qt * a.n_split;
   hipLaunchKernelGGL(cover_attn_rect_kernel, dim3((unsigned)nwg), dim3(kThreads), 0, stream, p);
   hipError_t e = hipGetLastError();

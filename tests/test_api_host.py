@@ -261,11 +261,23 @@ def test_attn_rect_rejects_bad_descriptors(kw, q_off, Lq, n_split, expect):
     assert _rect(cover.RectDesc(_good(**kw), q_off, Lq, n_split)) == expect
 
 
-def test_attn_rect_needs_a_workspace():
+def test_attn_rect_workspace_rules():
+    # key splits across workgroups need the caller's workspace; the single launch needs none
     assert _rect(None) == cover.COVER_ERR_INVALID
     assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=None) == cover.COVER_ERR_INVALID
     assert _rect(cover.RectDesc(_good(), 0, 8, 2), ws=FAKE + 4) == cover.COVER_ERR_INVALID
     assert cover.rect_workspace(1, 32, 256, 4) == 32 * 4 * 256 * cover.COVER_RECT_RECORD
+    assert cover.rect_workspace(1, 32, 256, 1) == 0
+    # single launch: a missing workspace passes validation (the stride limit is what fails)
+    big = _good(kv_sl=1 << 26, kv_sh=64 << 26, kv_sb=128 << 26)
+    assert _rect(cover.RectDesc(big, 0, 8, 1), ws=None) == cover.COVER_ERR_UNSUPPORTED
+
+
+def test_attn_rect_grid_limits():
+    # at most 2^32 work-items per launch: 2^23 - 8 workgroups of 512 for the single launch
+    huge = _good(B=1 << 20, Hq=8, Hkv=8)
+    assert _rect(cover.RectDesc(huge, 0, 64, 1), ws=None) == cover.COVER_ERR_UNSUPPORTED
+    assert _rect(cover.RectDesc(huge, 0, 64, 2)) == cover.COVER_ERR_UNSUPPORTED
 
 
 def test_token_sample_rejects_bad_arguments():

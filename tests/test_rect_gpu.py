@@ -95,3 +95,44 @@ def test_single_position_and_no_seeds():
     _check(a, 0, 1, where="L=1 seed")
     a = synth.attn_inputs("llada", seed=7)
     _check(a, 768, 256, seeds=False, where="no seeds")
+
+
+@pytest.mark.parametrize("case", ["llada256", "llada32", "llada64_896", "dream", "ragged",
+                                  "ragged_end", "all_seeds", "short", "L1", "no_seeds",
+                                  "long_seed_list", "batch_gqa"])
+def test_single_launch_form(case):
+    """n_split = 1: the single-launch kernel (key split across the waves of a workgroup,
+    merged in LDS), on every case shape above plus short sequences (waves without stages)
+    and seed lists longer than the part fetched into LDS."""
+    if case == "llada256":
+        _check(synth.attn_inputs("llada", seed=10), 768, 256, n_split=1, where=case)
+    elif case == "llada32":
+        _check(synth.attn_inputs("llada", seed=11), 992, 32, n_split=1, where=case)
+    elif case == "llada64_896":
+        _check(synth.attn_inputs("llada", seed=12), 896, 64, n_split=1, where=case)
+    elif case == "dream":
+        _check(synth.attn_inputs("dream", seed=13), 512, 256, n_split=1, where=case)
+    elif case == "ragged":
+        _check(_custom(14, 2, 4, 2, 1000, 0, positions=[5, 900, 910, 933, 976, 999]), 900, 77,
+               n_split=1, where=case)
+    elif case == "ragged_end":
+        _check(_custom(15, 2, 4, 2, 1000, 0, positions=[0, 31, 32, 923, 999]), 923, 77,
+               n_split=1, where=case)
+    elif case == "all_seeds":
+        _check(_custom(16, 1, 2, 2, 256, 0, positions=list(range(256))), 100, 100, n_split=1,
+               where=case)
+    elif case == "short":  # 4 stages for 8 waves; 3 stages, the last ragged
+        _check(_custom(17, 1, 2, 1, 100, 0, positions=[3, 50, 99]), 40, 60, n_split=1, where=case)
+        _check(_custom(18, 1, 2, 2, 70, 0, positions=[69]), 0, 70, n_split=1, where=case)
+    elif case == "L1":
+        _check(_custom(19, 1, 2, 2, 1, 0, positions=[0]), 0, 1, n_split=1, where=case)
+    elif case == "no_seeds":
+        _check(synth.attn_inputs("llada", seed=20), 768, 256, n_split=1, seeds=False, where=case)
+    elif case == "long_seed_list":  # 700 seeds: 512 through LDS, the rest by plain loads
+        rng = np.random.default_rng(21)
+        pos = rng.choice(1024, size=700, replace=False)
+        _check(_custom(21, 1, 2, 2, 1024, 0, positions=pos.tolist()), 600, 200, n_split=1,
+               where=case)
+    elif case == "batch_gqa":
+        _check(_custom(22, 3, 8, 2, 640, 0, positions=[1, 100, 333, 500, 639]), 480, 160,
+               n_split=1, where=case)
