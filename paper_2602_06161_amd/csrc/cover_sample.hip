@@ -9,7 +9,10 @@
 // token, step) has its own fixed random number whatever the launch shape.  Each thread keeps
 // the best perturbed score with its index and logit, and an online (max, sum of exp) of x/T;
 // the workgroup merges them (ties: smaller index).  HBM-bound in principle (one read of the
-// logits); the generator costs about 15 integer operations per token.
+// logits); in practice bound by the vector ALU: per 4 tokens ten Philox rounds of two
+// 32x32 -> 64-bit products (one v_mad_u64_u32 each) and their mixing, per token two
+// logarithms (the perturbed score is kept up to a constant that the argmax ignores) and one
+// exponential.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -47,8 +50,9 @@ __device__ __forceinline__ u32x4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
       k0 += 0x9E3779B9u;
       k1 += 0xBB67AE85u;
     }
-    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
-    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0, p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t lo0 = (uint32_t)p0, hi0 = (uint32_t)(p0 >> 32);
+    const uint32_t lo1 = (uint32_t)p1, hi1 = (uint32_t)(p1 >> 32);
     const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0;
     c1 = lo1;
@@ -58,23 +62,23 @@ __device__ __forceinline__ u32x4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
   return u32x4{c0, c1, c2, c3};
 }
 
-// standard Gumbel noise from one 32-bit word
-__device__ __forceinline__ float gumbel(uint32_t w) {
-  const float u = ((float)(w >> 9) + 0.5f) * 1.1920928955078125e-7f;  // 2^-23
-  const float nl = -__builtin_amdgcn_logf(u) * kLn2;                 // -ln u > 0
-  return -__builtin_amdgcn_logf(nl) * kLn2;
+// x / T plus Gumbel noise from one 32-bit word, up to a constant: -ln(-ln u) =
+// -ln2 log2(-log2 u) - ln(ln 2), and the constant, the same for every token, is dropped (the
+// argmax does not see it)
+__device__ __forceinline__ float perturbed(float z, uint32_t w) {
+  const float u = __builtin_fmaf((float)(w >> 9), 1.1920928955078125e-7f, 5.9604644775390625e-8f);  // ((w >> 9) + 1/2) 2^-23
+  return __builtin_fmaf(-kLn2, __builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)), z);
 }
 
 struct Acc {
-  float y;   // best perturbed score
+  float y;   // best perturbed score (up to the dropped constant)
   int i;     // its index
   float z;   // its x / T
   float m;   // max of x / T
   float s;   // sum of exp(x / T - m)
 };
 
-__device__ __forceinline__ void add(Acc& a, float z, float g, int v) {
-  const float y = z + g;
+__device__ __forceinline__ void add(Acc& a, float z, float y, int v) {
   if (y > a.y || (y == a.y && v < a.i)) {
     a.y = y;
     a.i = v;
@@ -119,13 +123,17 @@ __global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const Samp
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int v = 8 * c + 2 * e;
-        add(acc, bf_lo(raw[e]) * p.inv_t, gumbel(e < 2 ? w0[2 * e] : w1[2 * e - 4]), v);
-        add(acc, bf_hi(raw[e]) * p.inv_t, gumbel(e < 2 ? w0[2 * e + 1] : w1[2 * e - 3]), v + 1);
+        const float z0 = bf_lo(raw[e]) * p.inv_t, z1 = bf_hi(raw[e]) * p.inv_t;
+        add(acc, z0, perturbed(z0, e < 2 ? w0[2 * e] : w1[2 * e - 4]), v);
+        add(acc, z1, perturbed(z1, e < 2 ? w0[2 * e + 1] : w1[2 * e - 3]), v + 1);
       }
     } else {
       const u32x4 w = philox((uint32_t)c, r, p.step, 0u, p.k0, p.k1);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) add(acc, __uint_as_float(raw[e]) * p.inv_t, gumbel(w[e]), 4 * c + e);
+      for (int e = 0; e < 4; ++e) {
+        const float z = __uint_as_float(raw[e]) * p.inv_t;
+        add(acc, z, perturbed(z, w[e]), 4 * c + e);
+      }
     }
   }
   // the tail: one element per thread, read at its own width
@@ -133,7 +141,8 @@ __global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const Samp
     const int v = nfull * per + tid;
     const float x = p.bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
     const u32x4 w = philox((uint32_t)(v >> 2), r, p.step, 0u, p.k0, p.k1);
-    add(acc, x * p.inv_t, gumbel(w[v & 3]), v);
+    const float z = x * p.inv_t;
+    add(acc, z, perturbed(z, w[v & 3]), v);
   }
   // merge: across the wave, then the waves
 #pragma unroll
