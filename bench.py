@@ -828,10 +828,29 @@ def cpu_baseline(a: dict, flops: int) -> dict:
         t_total += time.perf_counter() - t0
         reps += 1
     per = t_total / reps
-    return {"value": round(flops / per / 1e12, 5), "unit": "TFLOP/s", "cores": oracle.threads(),
+    cores = oracle.threads()
+    # one core: the attention of one head (all L rows), about 2 s of repetitions
+    c = a["cfg"]
+    rows = np.arange(c.L, dtype=np.int64)
+    oracle.set_threads(1)
+    try:
+        reps1, t1 = 0, 0.0
+        while (t1 < 2.0 and reps1 < 100) or reps1 == 0:
+            t0 = time.perf_counter()
+            oracle.attn(*args, si, ns, scale=a["scale"], mode="fast", rows=rows)
+            t1 += time.perf_counter() - t0
+            reps1 += 1
+    finally:
+        oracle.set_threads(cores)
+    flops1 = 4 * c.L * c.L * c.d
+    return {"value": round(flops / per / 1e12, 5), "unit": "TFLOP/s", "cores": cores,
             "kind": "oracle", "seconds_per_step": round(per, 4),
-            "sample": f"{reps} full layer-steps (all {a['cfg'].Hq} heads x {a['cfg'].L} rows, fp64, "
-                      f"fast mode) + selection, {t_total:.1f} s total"}
+            "sample": f"{reps} full layer-steps (all {c.Hq} heads x {c.L} rows, fp64, "
+                      f"fast mode) + selection, {t_total:.1f} s total",
+            "single_core": {"value": round(flops1 * reps1 / t1 / 1e12, 6), "unit": "TFLOP/s",
+                            "cores": 1, "sample": f"{reps1} x the attention of one head "
+                                                  f"({c.L} rows x {c.L} keys, fp64, fast mode), "
+                                                  f"{t1:.1f} s"}}
 
 
 if __name__ == "__main__":

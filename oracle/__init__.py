@@ -67,6 +67,8 @@ def _load():
         lib.cover_oracle_attn_stats.argtypes = [P, P, P, P, P, I, I, I, I, I, I, D, I, I, P, P, P, P]
         lib.cover_oracle_threads.argtypes = []
         lib.cover_oracle_threads.restype = ctypes.c_int
+        lib.cover_oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.cover_oracle_set_threads.restype = None
         for f in (lib.cover_oracle_attn, lib.cover_oracle_attn_closed, lib.cover_oracle_select,
                   lib.cover_oracle_token_stats, lib.cover_oracle_attn_stats):
             f.restype = ctypes.c_int
@@ -77,6 +79,11 @@ def _load():
 def threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().cover_oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Sets the OpenMP threads of the oracle's parallel loops (results do not depend on it)."""
+    _load().cover_oracle_set_threads(int(n))
 
 
 def _f64(x) -> np.ndarray:

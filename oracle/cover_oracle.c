@@ -39,8 +39,12 @@
 #include <stdlib.h>
 #include <string.h>
 
-/* Threads the OpenMP loops below use (reported with CPU timings). */
+/* Threads the OpenMP loops below use (reported with CPU timings), and a way to set them
+ * (n > 0; for single-core timings).  Results do not depend on the count. */
 int cover_oracle_threads(void) { return omp_get_max_threads(); }
+void cover_oracle_set_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+}
 
 #define OR_OK 0
 #define OR_ERR_SIZE 1
