@@ -391,8 +391,9 @@ __global__ __launch_bounds__(256) void cover_attn_rect_merge_kernel(const RectPa
 // Single-launch form (n_split == 1): one workgroup of 8 waves per (batch, query head,
 // 32-query tile).  A CU's load path, not HBM, bounds a short block (about 100 GB/s per CU),
 // and the merge of key splits held by different workgroups costs a second launch; so the
-// key split stays inside the workgroup: wave w takes the w-th eighth of the 32-key stages
-// and streams them through a K slot and a V slot of its own by global-to-LDS loads (no
+// key split stays inside the workgroup: wave w takes a contiguous share of the 32-key
+// stages (the first four waves more than the other four, which issue their loads after
+// them) and streams them through a K slot and a V slot of its own by global-to-LDS loads (no
 // barrier in the loop), each slot refilled as soon as it has been read.  The eight partial
 // (max, sum, O) states and a seed row's live diagonal term are merged through LDS at the end.
 // Workgroups that share a KV head are placed on one XCD, so its L2 serves their re-reads.
@@ -487,7 +488,12 @@ __global__ __launch_bounds__(64 * kTW, 1) void cover_attn_tile_kernel(const Rect
   const int h = bh % p.Hq, b = bh / p.Hq, g = h / p.group;
   const int L = p.L;
   const int nst = (L + kStage - 1) / kStage;
-  const int s0 = wave * nst / kTW, s1 = (wave + 1) * nst / kTW;  // this wave's stages
+  // this wave's stages: waves 0-3 take 10/64 of them each, waves 4-7 (the second wave of
+  // each SIMD, which loses the load path's arbitration to the first) 6/64: the measured
+  // split that lets the waves finish together
+  const int cw0 = wave < 4 ? 10 * wave : 40 + 6 * (wave - 4);
+  const int cw1 = wave < 3 ? 10 * (wave + 1) : 40 + 6 * (wave - 3);
+  const int s0 = nst * cw0 / 64, s1 = nst * cw1 / 64;
   const int ragged = L % kStage ? nst - 1 : -1;
   const int nW = (L + 31) >> 5;
   for (int w = tid; w < nW; w += 64 * kTW) bits[w] = 0u;

@@ -136,3 +136,14 @@ def test_single_launch_form(case):
     elif case == "batch_gqa":
         _check(_custom(22, 3, 8, 2, 640, 0, positions=[1, 100, 333, 500, 639]), 480, 160,
                n_split=1, where=case)
+
+
+def test_single_launch_long_sequence():
+    """The single launch at L = 4200 (132 stages of 32 keys, 16-17 per wave, the last ragged)
+    with seeds in the first, middle and last stages and a block of 256 rows whose 256
+    workgroups keep the single launch the default form."""
+    pos = [0, 31, 1500, 2047, 2048, 2049, 3999, 4000, 4100, 4191, 4199]
+    a = _custom(23, 1, 32, 32, 4200, 0, positions=pos)
+    assert cover.rect_splits(1, 32, 256, 4200) == 1
+    _check(a, 3944, 256, where="L4200 block at the end")
+    _check(a, 1900, 64, n_split=1, where="L4200 middle block")
