@@ -7,9 +7,14 @@
 // other position's from the live tensors, and a seed row sees its own live key and value on
 // its diagonal (the leave-one-out view whose closed form App. B.4 gives).
 //
-// With few query rows the work is bound by reading K and V once, not by the MFMAs, and one
-// workgroup per (row, query tile) would leave most of the chip idle, so the keys are split:
-//   * kernel 1: one workgroup of 4 waves per (batch, query head, 128-query tile, key split).
+// With few query rows the work is bound by reading K and V, not by the MFMAs, and one
+// workgroup per (row, 128-query tile) would leave most of the chip idle, so the keys are
+// split.  Two forms:
+//   * n_split == 1, cover_attn_tile_kernel (the default up to L = 2048): one launch, one
+//     workgroup of 8 waves per 32 query rows whose waves split the keys among themselves
+//     and merge in LDS (described at the kernel, below).
+//   * n_split > 1, two launches through the caller's workspace:
+//   kernel 1: one workgroup of 4 waves per (batch, query head, 128-query tile, key split).
 //     The waves share the split's K/V in LDS, loaded in groups of up to four 32-key stages
 //     (128 keys, 64 KiB) that are all requested at once, so a group costs one memory round
 //     trip; wave w owns 32 queries.  The Q rows and the seed list are requested together at
