@@ -84,7 +84,8 @@ def main() -> int:
     ap.add_argument("--phase-timing", action="store_true",
                     help="run the attention kernel of the timing build of the library "
                          "(lib/libcover_timing.so) once after warm-up and print where a "
-                         "workgroup's cycles go, and the shader clock under load")
+                         "workgroup's cycles go, and the shader clock under load (with "
+                         "--workload block: the single-launch block attention kernel)")
     ap.add_argument("--kernel", choices=["token_stats", "token_sample", "attn_stats",
                                          "decode_update"], default=None)
     ap.add_argument("--lm-scale", type=float, default=8.0,
@@ -129,6 +130,8 @@ def main() -> int:
         return 0
 
     if args.phase_timing:
+        if args.workload == "block":
+            return bench_block_phase_timing(args, dev, stream)
         return bench_phase_timing(args, dev, stream)
     if args.calibrate_mfma:
         return bench_calibrate_mfma(args, dev, stream)
@@ -648,6 +651,69 @@ def bench_phase_timing(args, dev, stream) -> int:
         "step_cycles_median": steps,
     }
     print(json.dumps(rec))
+    return 0
+
+
+def bench_block_phase_timing(args, dev, stream) -> int:
+    """Per-phase cycle counts of cover_attn_tile_kernel (the single-launch block attention)
+    from its timing build, at the LLaDA-8B layer shape: blocks of 256 rows at 768 and 32 rows
+    at 992 with the workload's seeds, and 32 rows without seeds.  Medians over all waves of
+    all workgroups; per-stage cycles per wave (from its first stage's data to the end of its
+    loop, over its own number of stages), for waves 0-3 and 4-7 apart; the merge barrier's
+    wait and the workgroup total (first stamp to last)."""
+    import ctypes
+    import numpy as np
+    import torch
+    from paper_2602_06161_amd import cover, synth
+    from paper_2602_06161_amd.build import LIB_TIMING
+
+    cover.use_library(LIB_TIMING)
+    a = synth.attn_inputs("llada", seed=args.seed)
+    q, kl, vl, kc, vc, si, ns = (a[k].to(dev) for k in ("q", "k_live", "v_live", "k_cache",
+                                                         "v_cache", "seed_idx", "n_seed"))
+    B, H, L, d = a["q"].shape
+    WG, W, S = 1024, 8, 32
+    nst = -(-L // 32)
+    cw = [0, 10, 20, 30, 40, 46, 52, 58, 64]  # the kernel's stage split, in 64ths
+    n_w = np.array([nst * cw[w + 1] // 64 - nst * cw[w] // 64 for w in range(W)])
+    med = lambda x: float(np.median(x))
+    for Lq, q_off, seeded in ((256, 768, True), (32, 992, True), (32, 992, False)):
+        qb = q[:, :, q_off:q_off + Lq].contiguous()
+        call = cover.PreparedRect(qb, kl, vl, kc, vc, q_off, si if seeded else None,
+                                  ns if seeded else None, n_split=1, stream=stream)
+        for _ in range(max(1, args.warmup)):
+            call()
+        torch.cuda.synchronize()
+        call()
+        torch.cuda.synchronize()
+        buf = np.zeros(WG * W * S, dtype=np.uint64)
+        rc = cover.lib().cover_rect_timing_read(buf.ctypes.data_as(ctypes.c_void_p),
+                                                ctypes.c_int64(buf.size))
+        if rc != 0:
+            raise RuntimeError(f"cover_rect_timing_read failed ({rc})")
+        nwg = min(WG, B * H * -(-Lq // 32))
+        T = buf.reshape(WG, W, S)[:nwg].astype(np.int64)
+        per_stage = (T[:, :, 20] - T[:, :, 3]) / np.maximum(n_w, 1)[None, :]
+        rec = {
+            "phase_timing": f"block attention, LLaDA-8B layer B={B} H={H} L={L} d={d}, block of "
+                            f"{Lq} rows at {q_off}, {'%d seeds' % int(a['n_seed'][0]) if seeded else 'no seeds'}",
+            "workgroups": nwg, "stages_per_wave": n_w.tolist(),
+            "cycles_median": {
+                "seeds_and_q_landed": med(T[:, :, 1] - T[:, :, 0]),
+                "seed_bitmap": med(T[:, :, 2] - T[:, :, 1]),
+                "first_stage_landed": med(T[:, :, 3] - T[:, :, 2]),
+                "per_stage_waves_0_3": med(per_stage[:, :4]),
+                "per_stage_waves_4_7": med(per_stage[:, 4:]),
+                "merge_barrier_wait": med(T[:, :, 21] - T[:, :, 20]),
+                "merge": med(T[:, :, 22] - T[:, :, 21]),
+                "workgroup_total": med(T[:, :, 22].max(axis=1) - T[:, :, 0].min(axis=1)),
+            },
+            "cycles_max": {
+                "first_stage_landed": float((T[:, :, 3] - T[:, :, 2]).max()),
+                "merge_barrier_wait": float((T[:, :, 21] - T[:, :, 20]).max()),
+            },
+        }
+        print(json.dumps(rec), flush=True)
     return 0
 
 
