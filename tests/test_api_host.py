@@ -295,3 +295,15 @@ def test_token_sample_rejects_bad_arguments():
     assert call(good, logits=FAKE + 8) == cover.COVER_ERR_INVALID
     assert call(cover.TokenDesc(4, 1000, cover.COVER_BF16, 1004)) == cover.COVER_ERR_INVALID
     assert call(cover.TokenDesc(0, 1000, cover.COVER_BF16, 1008), logits=None, tok=None) == cover.COVER_OK
+
+
+def test_rect_split_choice():
+    # the single launch up to L = 2048, and past it whenever its workgroups fill the GPU
+    assert cover.rect_splits(1, 32, 256, 1024) == 1
+    assert cover.rect_splits(1, 32, 32, 2048) == 1
+    assert cover.rect_splits(1, 32, 256, 4200) == 1          # 256 workgroups of 32 rows
+    # long sequences with few rows: key splits across workgroups (at least 128 keys each)
+    n = cover.rect_splits(1, 4, 32, 8192)
+    assert 2 <= n <= 256 and -(-8192 // n) >= 128
+    assert cover.rect_splits(1, 1, 1, 4096) == 32            # 4096 / 128 keys per split
+    assert cover.rect_workspace(1, 4, 32, n) > 0 and cover.rect_workspace(1, 4, 32, 1) == 0
