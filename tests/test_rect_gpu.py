@@ -147,3 +147,34 @@ def test_single_launch_long_sequence():
     assert cover.rect_splits(1, 32, 256, 4200) == 1
     _check(a, 3944, 256, where="L4200 block at the end")
     _check(a, 1900, 64, n_split=1, where="L4200 middle block")
+
+
+@pytest.mark.parametrize("n_split", [1, 3])
+def test_distinct_seed_lists_per_batch_row(n_split):
+    """Each batch row has its own seed list and count: none, a few in and out of the block,
+    and a long list with entries past its count (padded with -1, ignored)."""
+    L, ms = 700, 40
+    cfg = synth.AttnConfig("custom", 3, 4, 2, L, 128, "bf16", 0, L, ms, "independent")
+    a = synth.attn_inputs(cfg, seed=24)
+    rng = np.random.default_rng(24)
+    si = np.full((3, ms), -1, np.int32)
+    counts = [0, 5, 33]
+    si[1, :5] = [0, 333, 500, 517, 699]
+    si[2, :33] = np.sort(rng.choice(L, size=33, replace=False))
+    si[2, 33:] = rng.choice(L, size=ms - 33)  # past the count: must be ignored
+    a["seed_idx"] = torch.from_numpy(si)
+    a["n_seed"] = torch.tensor(counts, dtype=torch.int32)
+    osi = torch.from_numpy(np.where(np.arange(ms)[None, :] < np.array(counts)[:, None], si, -1).astype(np.int32))
+    q, kl, vl, kc, vc, sid, nsd = to_dev(a)
+    q_off, Lq = 480, 150
+    announce(f"rect distinct seeds per row n_split={n_split}")
+    qb = q[:, :, q_off:q_off + Lq].contiguous()
+    out, lse = cover.cover_attn_rect(qb, kl, vl, kc, vc, q_off, sid, nsd, n_split=n_split)
+    torch.cuda.synchronize()
+    B, Hq, _, d = a["q"].shape
+    rows = np.array([(b * Hq + h) * L + i for b in range(B) for h in range(Hq)
+                     for i in range(q_off, q_off + Lq)], np.int64)
+    ref_o, ref_l = oracle.attn(a["q"], a["k_live"], a["v_live"], a["k_cache"], a["v_cache"], osi,
+                               a["n_seed"], scale=a["scale"], mode="fast", rows=rows)
+    check_attn(out, lse, ref_o.reshape(B, Hq, Lq, d), ref_l.reshape(B, Hq, Lq), torch.bfloat16,
+               "distinct seeds")
