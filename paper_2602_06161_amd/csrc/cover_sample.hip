@@ -6,13 +6,12 @@
 //   p     = softmax(x / T) at the token (the confidence the drafting threshold compares)
 // u_v is word v % 4 of Philox4x32-10 (Salmon et al., SC 2011) at counter (v / 4, row, step, 0)
 // and key (seed mod 2^32, seed / 2^32), mapped to ((w >> 9) + 1/2) 2^-23, so every (row,
-// token, step) has its own fixed random number whatever the launch shape.  Each thread keeps
-// the best perturbed score with its index and logit, and an online (max, sum of exp) of x/T;
-// the workgroup merges them (ties: smaller index).  HBM-bound in principle (one read of the
-// logits); in practice bound by the vector ALU: per 4 tokens ten Philox rounds of two
-// 32x32 -> 64-bit products (one v_mad_u64_u32 each) and their mixing, per token two
-// logarithms (the perturbed score is kept up to a constant that the argmax ignores) and one
-// exponential.
+// token, step) has its own fixed random number whatever the launch shape.  The argmax is
+// taken as the equivalent exponential race (below).  Each thread keeps its best token (with
+// its logit) and an online (max, sum of exp) of x/T; the workgroup merges them (ties: smaller
+// index).  HBM-bound in principle (one read of the logits); in practice bound by the vector
+// ALU: per 4 tokens ten Philox rounds of two 32x32 -> 64-bit products (one v_mad_u64_u32
+// each) and their mixing, per token one logarithm and one exponential.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -62,46 +61,57 @@ __device__ __forceinline__ u32x4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
   return u32x4{c0, c1, c2, c3};
 }
 
-// x / T plus Gumbel noise from one 32-bit word, up to a constant: -ln(-ln u) =
-// -ln2 log2(-log2 u) - ln(ln 2), and the constant, the same for every token, is dropped (the
-// argmax does not see it)
-__device__ __forceinline__ float perturbed(float z, uint32_t w) {
+// The Gumbel-max draw argmax_v (z_v - ln(-ln u_v)), z = x / T, as an exponential race:
+// with e_v = exp(z_v - m) (any common m) and E_v = -log2 u_v (ln 2 times an Exp(1) variable),
+// it is argmax_v e_v / E_v, compared by cross-multiplication; e_v is also the term of the
+// softmax sum, so a token costs one logarithm and one exponential.
+__device__ __forceinline__ float race_e(uint32_t w) {  // -log2 u > 0
   const float u = __builtin_fmaf((float)(w >> 9), 1.1920928955078125e-7f, 5.9604644775390625e-8f);  // ((w >> 9) + 1/2) 2^-23
-  return __builtin_fmaf(-kLn2, __builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)), z);
+  return -__builtin_amdgcn_logf(u);
 }
 
 struct Acc {
-  float y;   // best perturbed score (up to the dropped constant)
+  float be;  // e of the best token so far (relative to m)
+  float bE;  // its E
   int i;     // its index
   float z;   // its x / T
   float m;   // max of x / T
   float s;   // sum of exp(x / T - m)
 };
 
-__device__ __forceinline__ void add(Acc& a, float z, float y, int v) {
-  if (y > a.y || (y == a.y && v < a.i)) {
-    a.y = y;
+// tokens reach a thread in increasing order: a tie keeps the earlier (smaller) index
+__device__ __forceinline__ void add(Acc& a, float z, float E, int v) {
+  if (z > a.m) {
+    const float r = __builtin_amdgcn_exp2f((a.m - z) * kLog2e);
+    a.s *= r;
+    a.be *= r;
+    a.m = z;
+  }
+  const float e = __builtin_amdgcn_exp2f((z - a.m) * kLog2e);
+  a.s += e;
+  if (e * a.bE > a.be * E) {
+    a.be = e;
+    a.bE = E;
     a.i = v;
     a.z = z;
   }
-  if (z > a.m) {
-    a.s = a.s * __builtin_amdgcn_exp2f((a.m - z) * kLog2e);
-    a.m = z;
-  }
-  a.s += __builtin_amdgcn_exp2f((z - a.m) * kLog2e);
 }
 
-__device__ __forceinline__ Acc merge(Acc a, const Acc& b) {
-  if (b.y > a.y || (b.y == a.y && b.i < a.i)) {
-    a.y = b.y;
+__device__ __forceinline__ Acc merge(Acc a, Acc b) {
+  const float m = fmaxf(a.m, b.m);
+  const float ra = a.m == m ? 1.0f : __builtin_amdgcn_exp2f((a.m - m) * kLog2e);
+  const float rb = b.m == m ? 1.0f : __builtin_amdgcn_exp2f((b.m - m) * kLog2e);
+  a.s = a.s * ra + b.s * rb;
+  a.be *= ra;
+  b.be *= rb;
+  a.m = m;
+  const float l = b.be * a.bE, rgt = a.be * b.bE;  // b better: b.be / b.bE > a.be / a.bE
+  if (l > rgt || (l == rgt && b.i < a.i)) {
+    a.be = b.be;
+    a.bE = b.bE;
     a.i = b.i;
     a.z = b.z;
   }
-  const float m = fmaxf(a.m, b.m);
-  const float sa = a.s == 0.0f ? 0.0f : a.s * __builtin_amdgcn_exp2f((a.m - m) * kLog2e);
-  const float sb = b.s == 0.0f ? 0.0f : b.s * __builtin_amdgcn_exp2f((b.m - m) * kLog2e);
-  a.m = m;
-  a.s = sa + sb;
   return a;
 }
 
@@ -114,7 +124,7 @@ __global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const Samp
   const char* row = p.logits + (int64_t)r * p.row_stride_bytes;
   const int per = p.bf16 ? 8 : 4;  // elements per 16-byte chunk
   const int nfull = p.V / per;
-  Acc acc = {-INFINITY, 0x7fffffff, 0.0f, -INFINITY, 0.0f};
+  Acc acc = {0.0f, 1.0f, 0x7fffffff, 0.0f, -INFINITY, 0.0f};
   for (int c = tid; c < nfull; c += kThreads) {
     const u32x4 raw = *(gu32x4*)((__attribute__((address_space(1))) const char*)row + (int64_t)c * 16);
     if (p.bf16) {
@@ -123,17 +133,13 @@ __global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const Samp
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int v = 8 * c + 2 * e;
-        const float z0 = bf_lo(raw[e]) * p.inv_t, z1 = bf_hi(raw[e]) * p.inv_t;
-        add(acc, z0, perturbed(z0, e < 2 ? w0[2 * e] : w1[2 * e - 4]), v);
-        add(acc, z1, perturbed(z1, e < 2 ? w0[2 * e + 1] : w1[2 * e - 3]), v + 1);
+        add(acc, bf_lo(raw[e]) * p.inv_t, race_e(e < 2 ? w0[2 * e] : w1[2 * e - 4]), v);
+        add(acc, bf_hi(raw[e]) * p.inv_t, race_e(e < 2 ? w0[2 * e + 1] : w1[2 * e - 3]), v + 1);
       }
     } else {
       const u32x4 w = philox((uint32_t)c, r, p.step, 0u, p.k0, p.k1);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float z = __uint_as_float(raw[e]) * p.inv_t;
-        add(acc, z, perturbed(z, w[e]), 4 * c + e);
-      }
+      for (int e = 0; e < 4; ++e) add(acc, __uint_as_float(raw[e]) * p.inv_t, race_e(w[e]), 4 * c + e);
     }
   }
   // the tail: one element per thread, read at its own width
@@ -141,14 +147,14 @@ __global__ __launch_bounds__(kThreads) void cover_token_sample_kernel(const Samp
     const int v = nfull * per + tid;
     const float x = p.bf16 ? __uint_as_float((uint32_t)((const uint16_t*)row)[v] << 16) : ((const float*)row)[v];
     const u32x4 w = philox((uint32_t)(v >> 2), r, p.step, 0u, p.k0, p.k1);
-    const float z = x * p.inv_t;
-    add(acc, z, perturbed(z, w[v & 3]), v);
+    add(acc, x * p.inv_t, race_e(w[v & 3]), v);
   }
   // merge: across the wave, then the waves
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     Acc b;
-    b.y = __shfl_xor(acc.y, o);
+    b.be = __shfl_xor(acc.be, o);
+    b.bE = __shfl_xor(acc.bE, o);
     b.i = __shfl_xor(acc.i, o);
     b.z = __shfl_xor(acc.z, o);
     b.m = __shfl_xor(acc.m, o);
