@@ -222,9 +222,9 @@ __device__ uint64_t g_attn_times[kTimeWG * kWaves * kTimeSlots];
 #endif
 
 __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params4 p) {
-  // Three K and three V stage buffers; Q of the workgroup on its way to registers (at the end:
-  // the live key rows of the seed rows' diagonals); the seed list, the seed bitmap of the
-  // sequence and its per-stage summary; merge scalars; the recompute flag.
+  // Three K and three V stage buffers; Q of the workgroup on its way to registers (later: the
+  // live rows of the seed rows' diagonals, then the output tiles); the seed list, the seed
+  // bitmap of the sequence and its per-stage summary; merge scalars; the recompute flag.
   __shared__ __attribute__((aligned(1024))) char sK0[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sK1[kSBytes];
   __shared__ __attribute__((aligned(1024))) char sK2[kSBytes];
@@ -722,17 +722,54 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     float acc = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
-      const u32x4 kv = dkr[ks];
-      const u32x4 qv = __builtin_bit_cast(u32x4, qa[0][ks]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc = __builtin_fmaf(bf16_lo(qv[e]), bf16_lo(kv[e]), acc);
-        acc = __builtin_fmaf(bf16_hi(qv[e]), bf16_hi(kv[e]), acc);
-      }
+      const bf16x8 kv = __builtin_bit_cast(bf16x8, dkr[ks]);
+      const bf16x8 qv = qa[0][ks];
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(qv, qv, 0, 1), __builtin_shufflevector(kv, kv, 0, 1), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(qv, qv, 2, 3), __builtin_shufflevector(kv, kv, 2, 3), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(qv, qv, 4, 5), __builtin_shufflevector(kv, kv, 4, 5), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(qv, qv, 6, 7), __builtin_shufflevector(kv, kv, 6, 7), acc, false);
     }
     return swap_add(acc);
   };
   float s_live = 0.0f;
+  // The seed rows among the finished tile's queries (its 32 positions are bitmap word qd0 / 32):
+  // their live key and value rows go to this wave's 8 KiB of the Q area (free from the first
+  // step until the output tile is staged there) by global-to-LDS loads, four rows per load,
+  // issued with the last step; slot k holds the k-th seed row (key at 256 k, value at 4096 +
+  // 256 k).  A tile with more than 16 seed rows (or a sequence without steps) loads the rows
+  // of all its queries into registers instead.
+  const uint32_t dmask = block_seeded ? bits[qd0 >> 5] : 0u;
+  const bool diag_lds = __builtin_popcount(dmask) <= 16 && last > 0;
+  lds_t* const dgA = (lds_t*)sQ + wave * (32 * kRow);
+  auto issue_diag = [&]() __attribute__((always_inline)) {
+    uint32_t msk = dmask;
+    for (int u = 0; msk; ++u) {
+      int r = -1;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        if (msk) {
+          const int b = __builtin_ctz(msk);
+          msk &= msk - 1;
+          if ((lane >> 4) == g) r = b;
+        }
+      }
+      if (r >= 0) {
+        const int64_t src = (int64_t)(qd0 + r) * row_bytes + ((lane & 15) << 4);
+        dma16(lds_u32(dgA + u * 1024), klb + src);
+        dma16(lds_u32(dgA + 4096 + u * 1024), vlb + src);
+      }
+    }
+  };
+  // this lane's query's slot (meaningful for seed rows only)
+  const int dslot = __builtin_popcount(dmask & ((1u << l32) - 1u));
+  auto diag_from_lds = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) dkr[ks] = lds_read16(dgA + dslot * kRow + (2 * ks + hl) * 16);
+#pragma unroll
+    for (int c = 0; c < kDB * 4; ++c)
+      dvr[c] = qd_seed ? *(const __attribute__((address_space(3))) u32x2*)(dgA + 4096 + dslot * kRow + 16 * c + 8 * hl)
+                       : (u32x2){0u, 0u};
+  };
   uint64_t win = flags_at(0);  // the row-by-row flags of stages (i & ~31) + 0 .. 63
   auto step = [&](auto ph) __attribute__((always_inline)) -> bool {
     constexpr int P = decltype(ph)::value;
@@ -756,6 +793,16 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
       if (i + 2 < n_it) patch(kbuf((P + 2) % 3), klb, kcb, offK, i + 2);
       patch(vbuf((P + 1) % 3), vlb, vcb, offV, i + 1);
     }
+    // a seeded tile's live diagonal key and value rows go out with the last step, so that
+    // they have landed by the last stage and the finish
+    if (__builtin_expect(block_seeded && i == last - 1, 0)) {
+      if (diag_lds) {
+        issue_diag();
+      } else {
+        load_diag_k();
+        load_diag_v();
+      }
+    }
     bad |= fused(kbuf((P + 1) % 3), sn, sc, vbuf(P % 3), kbuf(P % 3), kg, vbuf((P + 2) % 3), vg);
     ++i;
     return false;
@@ -769,21 +816,24 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     if (step(IC<5>{})) break;
   }
   // Last stage: its S is in sA or sB by parity (selected by value: a selected pointer would
-  // send the tiles through memory), V in buffer last % 3.  Seeded waves load their diagonal
-  // key rows here, so the loads overlap the last softmax and PV product.
+  // send the tiles through memory), V in buffer last % 3.  Seeded waves issued their diagonal
+  // key and value rows with the last step (here, if there was none).
   {
     f32x16 sc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) sc[t] = (last & 1) ? sB[t] : sA[t];
     if (is_special(last)) special_fix(last, sc);
     // V(last) and its re-loaded rows were issued two steps and one step ago; the eight loads
-    // of the previous step (stages past the end) and the diagonal key rows issued here may stay
-    // in flight (loads complete in order).  Every load has landed before the buffers are
+    // of the previous step (stages past the end) and the diagonal rows issued before them may
+    // stay in flight (loads complete in order).  Every load has landed before the buffers are
     // reused after this block.
-    if (block_seeded) {
+    if (block_seeded && last == 0) {  // (no steps: the diagonal rows are loaded here)
       load_diag_k();
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads + kKS));
-    } else {
+      load_diag_v();
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    } else if (block_seeded && !diag_lds) {  // the diagonal rows and the previous step's loads may fly
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads + kKS + kDB * 4));
+    } else {  // (the diagonal rows' global-to-LDS loads, issued a step ago, land here too)
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kLoads));
     }
     __builtin_amdgcn_s_barrier();
@@ -792,7 +842,10 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     bad |= softmax(sc, pk, m);
     const int vb = last % 3;
     pv(vbuf(0) + (vb == 0 ? 0 : (vb == 1 ? (int)(vbuf(1) - vbuf(0)) : (int)(vbuf(2) - vbuf(0)))), pk, IC<4>{});
-    if (block_seeded) s_live = live_score();  // the key rows' load overlapped the last stage
+    if (block_seeded) {
+      if (diag_lds) diag_from_lds();
+      s_live = live_score();
+    }
     COVER_TSTAMP(71);
   }
   if (bad) atomicOr(&sbad, 1u);
@@ -856,7 +909,6 @@ __global__ __launch_bounds__(kThreads, 1) void cover_attn_w4_kernel(const Params
     }
   sML[(wave * 2 + 0) * 64 + lane] = m[1];
   sML[(wave * 2 + 1) * 64 + lane] = l_tot1;
-  if (block_seeded) load_diag_v();  // the seed rows' live values, for the finish
   __syncthreads();
   COVER_TSTAMP(73);
   // The finished tile: O^T entry (db, j) of lane (l32, hl) is column l32 (query qd0 + l32),
