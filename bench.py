@@ -86,6 +86,8 @@ def main() -> int:
                          "(lib/libcover_timing.so) once after warm-up and print where a "
                          "workgroup's cycles go, and the shader clock under load (with "
                          "--workload block: the single-launch block attention kernel)")
+    ap.add_argument("--zero-seeds", action="store_true",
+                    help="with --phase-timing: the same attention launch with empty seed lists")
     ap.add_argument("--kernel", choices=["token_stats", "token_sample", "attn_stats",
                                          "decode_update"], default=None)
     ap.add_argument("--lm-scale", type=float, default=8.0,
@@ -599,6 +601,8 @@ def bench_phase_timing(args, dev, stream) -> int:
     cover.use_library(LIB_TIMING)
     a = synth.attn_inputs(args.workload, seed=args.seed)
     c = a["cfg"]
+    if args.zero_seeds:  # the same launch with empty seed lists (what the seeds cost)
+        a["n_seed"] = a["n_seed"] * 0
     t = {k: a[k].to(dev) for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx",
                                    "n_seed")}
     attn = cover.PreparedAttn(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
@@ -640,6 +644,20 @@ def bench_phase_timing(args, dev, stream) -> int:
     steps = [med(T[:, :, 7 + i] - T[:, :, 6 + i]) for i in range(min(n_it - 2, 63))]
     tot = phases["total"].max(axis=1)
     slow = int(np.argmax(tot))
+    # workgroups whose own 128 query rows hold seeds (logical index: query tile li % n_qt of
+    # batch row li // (Hq n_qt)) against the others: the launch ends with the slowest
+    seeded = np.zeros(nwg, dtype=bool)
+    si, ns = a["seed_idx"].numpy(), a["n_seed"].numpy()
+    for li in range(nwg):
+        b, qt = li // (c.Hq * n_qt), li % n_qt
+        pos = si[b, : ns[b]]
+        seeded[li] = bool(((pos >= qt * 128) & (pos < qt * 128 + 128)).any())
+    split = {}
+    for name, sel in (("seeded", seeded), ("other", ~seeded)):
+        if sel.any():
+            split[name] = {"workgroups": int(sel.sum()),
+                           "total_cycles_median": med(tot[sel]),
+                           "phase_cycles_median": {k: med(v[sel]) for k, v in phases.items()}}
     rec = {
         "phase_timing": f"{args.workload}: B={c.B} Hq={c.Hq} Hkv={c.Hkv} L={c.L} d={c.d}",
         "workgroups": nwg,
@@ -649,6 +667,7 @@ def bench_phase_timing(args, dev, stream) -> int:
         "cycles_slowest_workgroup": {k: float(v[slow].max()) for k, v in phases.items()},
         "slowest_workgroup": slow,
         "step_cycles_median": steps,
+        "seeded_vs_other_workgroups": split,
     }
     print(json.dumps(rec))
     return 0
