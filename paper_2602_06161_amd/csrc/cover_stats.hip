@@ -254,24 +254,51 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
   float* const wsh = p.ws + ((int64_t)b * p.Hq + h) * (1 + p.KG) * p.Lr;
   const int g = h / p.group;
   const int L = p.L;
+  const __bf16* qbh = p.q + b * p.q_sb + h * p.q_sh;
+  const int64_t kvo = b * p.kv_sb + g * p.kv_sh;
+  const float* lrow = p.lse + ((int64_t)b * p.Hq + h) * L;
+  const float scale = p.scale;
+  // Everything that does not depend on the seed set is requested before the seed bitmap is
+  // built (the kernel is latency bound: a few dependent memory round trips): the seed count
+  // with the first 512 seed positions, and for this wave's first query block its Q rows,
+  // membership flags and lse, and the drafted flags of the group's first key tile.
+  const int ns_raw = p.max_seeds > 0 ? p.n_seed[b] : 0;
+  const int j_first = tid < p.max_seeds ? p.seed_idx[(int64_t)b * p.max_seeds + tid] : -1;
+  // one query block's operands: Q (query qi, d-chunk 2ks+hl; also the A operand of S = Q K^T),
+  // its membership flag byte, the lse of the lane's query and of the queries in S's registers
+  bf16x8 qf[KS];
+  uint8_t mq_byte = 0;
+  float lse_own = 0.0f, lse_r[16];
+  auto load_block = [&](int qb) {
+    const int rb = qb * 32, qn = min(32, p.Lr - rb);
+    const int qi = p.r0 + rb + min(l32, qn - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qbh + (int64_t)qi * p.q_sl + (2 * ks + hl) * 8);
+    mq_byte = p.masked[(int64_t)b * p.Lr + rb + min(l32, qn - 1)];
+    lse_own = lrow[qi];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) lse_r[r] = lrow[p.r0 + rb + min(8 * (r >> 2) + 4 * hl + (r & 3), qn - 1)];
+  };
+  auto drafted_byte = [&](int kt) -> uint8_t {
+    const int kb = kt * 32, kn = min(32, p.Lr - kb);
+    return p.drafted[(int64_t)b * p.Lr + kb + min(l32, kn - 1)];
+  };
+  if (wave < p.NB) load_block(wave);
+  const uint8_t dk_first = kt0 < kt1 ? drafted_byte(kt0) : (uint8_t)0;
   // seed bitmap of this sequence; the d_in rows start at zero
   const int nwords = (L + 31) >> 5;
   for (int w = tid; w < nwords; w += 64 * kStatWaves) bits[w] = 0u;
   for (int j = lane; j < p.Lr; j += 64) sdin[wave][j] = 0.0f;
   __syncthreads();
-  int ns = p.max_seeds > 0 ? p.n_seed[b] : 0;
-  ns = ns < 0 ? 0 : (ns > p.max_seeds ? p.max_seeds : ns);
-  for (int t = tid; t < ns; t += 64 * kStatWaves) {
+  const int ns = ns_raw < 0 ? 0 : (ns_raw > p.max_seeds ? p.max_seeds : ns_raw);
+  if (tid < ns && (unsigned)j_first < (unsigned)L) atomicOr(&bits[j_first >> 5], 1u << (j_first & 31));
+  for (int t = tid + 64 * kStatWaves; t < ns; t += 64 * kStatWaves) {  // long seed lists
     const int j = p.seed_idx[(int64_t)b * p.max_seeds + t];
     if ((unsigned)j < (unsigned)L) atomicOr(&bits[j >> 5], 1u << (j & 31));
   }
   __syncthreads();
   auto is_seed = [&](int j) -> bool { return (bits[j >> 5] >> (j & 31)) & 1u; };
 
-  const __bf16* qbh = p.q + b * p.q_sb + h * p.q_sh;
-  const int64_t kvo = b * p.kv_sb + g * p.kv_sh;
-  const float* lrow = p.lse + ((int64_t)b * p.Hq + h) * L;
-  const float scale = p.scale;
   // the K rows of key tile kt (this lane's row, d-chunks 2ks+hl; seeds from the cache)
   auto load_k = [&](bf16x8* kf, int kt) {
     const int kb = kt * 32;
@@ -282,13 +309,14 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
     for (int ks = 0; ks < KS; ++ks) kf[ks] = *(const bf16x8*)(ksrc + (2 * ks + hl) * 8);
   };
   for (int qb = wave; qb < p.NB; qb += kStatWaves) {
+    if (qb != wave) load_block(qb);  // (the first block's operands were requested above)
     const int rb = qb * 32;                       // region offset of this query block
     const int qn = min(32, p.Lr - rb);            // queries of the block inside the region
     const int qi = p.r0 + rb + min(l32, qn - 1);  // this lane's query (clamped)
-    // Q operand: query qi, d-chunk 2ks+hl (also the A operand of S = Q K^T)
-    bf16x8 qf[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *(const bf16x8*)(qbh + (int64_t)qi * p.q_sl + (2 * ks + hl) * 8);
+    // the first key tile's rows go out before the live diagonal row below, so that the two
+    // round trips overlap
+    bf16x8 kf[KS], kn_f[KS];
+    if (kt0 < kt1) load_k(kf, kt0);
     // live diagonal score of this lane's position, for seed rows
     float s_live = 0.0f;
     const bool own_seed = l32 < qn && is_seed(qi);
@@ -303,15 +331,9 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
       }
       s_live = acc + __shfl_xor(acc, 32);
     }
-    // membership bits of the block's queries, and lse of the queries in S's registers
-    const uint64_t mq = __builtin_amdgcn_ballot_w64(l32 < qn && p.masked[(int64_t)b * p.Lr + rb + min(l32, qn - 1)] != 0) & 0xffffffffull;
-    const float lse_own = lrow[qi];
-    float lse_r[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) lse_r[r] = lrow[p.r0 + rb + min(8 * (r >> 2) + 4 * hl + (r & 3), qn - 1)];
+    // membership bits of the block's queries
+    const uint64_t mq = __builtin_amdgcn_ballot_w64(l32 < qn && mq_byte != 0) & 0xffffffffull;
     float dout = 0.0f;  // this lane's query: sum over drafted keys (its 16 of each tile)
-    bf16x8 kf[KS], kn_f[KS];
-    if (kt0 < kt1) load_k(kf, kt0);
     for (int kt = kt0; kt < kt1; ++kt) {
       if (kt + 1 < kt1) load_k(kn_f, kt + 1);  // the next tile's rows are requested first
       const int kb = kt * 32;
@@ -322,7 +344,8 @@ __global__ __launch_bounds__(64 * kStatWaves) void cover_attn_stats_kernel(const
         st = mfma16(kf[ks], qf[ks], st);
         sq = mfma16(qf[ks], kf[ks], sq);
       }
-      const uint64_t dk = __builtin_amdgcn_ballot_w64(l32 < kn && p.drafted[(int64_t)b * p.Lr + kb + min(l32, kn - 1)] != 0) & 0xffffffffull;
+      const uint8_t dkb = kt == kt0 ? dk_first : drafted_byte(kt);
+      const uint64_t dk = __builtin_amdgcn_ballot_w64(l32 < kn && dkb != 0) & 0xffffffffull;
       const bool diag_tile = kt == qb;
       float din = 0.0f;  // this lane's key: sum over masked queries (its 16 of the block)
 #pragma unroll
