@@ -137,6 +137,38 @@ def test_attn_stats_key_groups(B, Hq, Hkv, L, r0, Lr):
     _stats_case(a, r0, masked, drafted)
 
 
+def test_attn_stats_long_seed_lists():
+    """Seed lists longer than the 512 positions fetched with the seed count (the rest are read
+    in a loop), with entries outside [0, L) inside the count and junk past it (ignored), and a
+    batch row without seeds; the oracle gets the cleaned lists."""
+    B, Hq, Hkv, L, r0, Lr, ms = 2, 4, 2, 1100, 100, 900, 800
+    announce(f"attn stats long seed lists B{B} Hq{Hq} L{L} max_seeds {ms}")
+    a = synth.attn_inputs("tiny", seed=77, max_seeds=ms, B=B, Hq=Hq, Hkv=Hkv, L=L, d=128,
+                          dtype="bf16", prompt=0, unmasked_gen=L, n_seeds=0)
+    rng = np.random.default_rng(77)
+    si = rng.integers(-50, L + 50, size=(B, ms)).astype(np.int32)  # junk everywhere
+    good = np.sort(rng.choice(L, size=700, replace=False)).astype(np.int32)
+    si[0, :700] = good
+    si[0, 700:703] = [-5, L, L + 9]  # inside the count, outside [0, L)
+    counts = np.array([703, 0], np.int32)
+    clean = np.full((B, ms), -1, np.int32)
+    clean[0, :700] = good
+    a["seed_idx"], a["n_seed"] = torch.from_numpy(si), torch.from_numpy(counts)
+    masked = (rng.integers(0, 2, (B, Lr))).astype(np.uint8)
+    drafted = (rng.integers(0, 4, (B, Lr)) == 0).astype(np.uint8)
+    t = {k: a[k].cuda() for k in ("q", "k_live", "v_live", "k_cache", "v_cache", "seed_idx", "n_seed")}
+    _, lse = cover.cover_attn_fwd(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
+                                  t["seed_idx"], t["n_seed"])
+    m, d = torch.as_tensor(masked).cuda(), torch.as_tensor(drafted).cuda()
+    d_in, d_out = cover.cover_attn_stats(t["q"], t["k_live"], t["k_cache"], t["seed_idx"],
+                                         t["n_seed"], lse, m, d, r0)
+    torch.cuda.synchronize()
+    r_in, r_out = oracle.attn_stats(a["q"], a["k_live"], a["k_cache"], clean,
+                                    np.array([700, 0], np.int32), r0, masked, drafted)
+    np.testing.assert_allclose(d_in.cpu().numpy(), r_in, rtol=MASS_RTOL, atol=MASS_ATOL)
+    np.testing.assert_allclose(d_out.cpu().numpy(), r_out, rtol=MASS_RTOL, atol=MASS_ATOL)
+
+
 def test_attn_stats_workspace_checked():
     """A caller workspace smaller than the launch needs, or of the wrong dtype, is refused
     before anything is enqueued."""
