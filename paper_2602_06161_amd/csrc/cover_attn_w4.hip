@@ -19,7 +19,8 @@
 //   * The 128 O^T accumulators per lane and Q live in AGPRs (one wave per SIMD has 512
 //     registers); S, P and the operands read from LDS stay in VGPRs.
 //   * Every global load goes straight to LDS (global_load_lds_dwordx4): the seed list, Q (read
-//     into registers once), and K/V stages in three buffers each, issued two stages ahead and
+//     into registers once), the live rows of a seeded tile's diagonal (with the last step, into
+//     the Q area), and K/V stages in three buffers each, issued two stages ahead and
 //     spread between the MFMAs (a burst of them stalls the issuing wave on the vector-memory
 //     queue).  A stage is loaded from the live tensors through one scalar base; the rows that
 //     need another source (seed rows from the cache, rows of a ragged last stage) are loaded
@@ -129,8 +130,10 @@ __device__ __forceinline__ i16x4 v_tr(const lds_t* p) {
 
 // Global -> LDS loads as inline assembly: lane l's bytes land at LDS byte lds + 16 l (or + 4 l
 // for the dword form); lds is wave-uniform.  Every global load of this kernel takes this path
-// (apart from seed lists longer than 256 entries), so the compiler tracks none of them: every
-// read of their data is preceded by an explicit vmcnt wait of the issuing wave and a barrier.
+// (apart from seed lists longer than 256 entries and the register loads of the live diagonal
+// rows of a tile with more than 16 seed rows), so the compiler tracks none of them: every read
+// of their data is preceded by an explicit vmcnt wait of the issuing wave (and a barrier where
+// other waves' loads are read).
 __device__ __forceinline__ uint32_t lds_u32v(const lds_t* ptr) { return (uint32_t)(uintptr_t)ptr; }
 __device__ __forceinline__ uint32_t lds_u32(const lds_t* ptr) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ptr);
