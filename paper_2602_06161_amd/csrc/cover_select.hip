@@ -172,29 +172,52 @@ __global__ __launch_bounds__(kMaxThreads) void cover_select_kernel(const SelPara
 // ---------------------------------------------------------------------------------------
 constexpr int kWaveMaxPer = 16;  // 64 lanes x 16 = 1024 positions
 
-// DPP full-wave reductions (result valid in lane 63): quad xor 1 and 2, half-row and row
-// mirrors, then row broadcasts 15 and 31.
-template <int CTRL, int RMASK>
-__device__ __forceinline__ double dpp_f64(double x) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, x);
-  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)u, (int)(uint32_t)u, CTRL, RMASK, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(u >> 32), (int)(uint32_t)(u >> 32), CTRL, RMASK, 0xF, false);
-  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+// Full-wave butterflies of 32-bit values (the result in every lane): quad xor 1 and 2,
+// half-row and row mirrors (each pairs two groups of equal size), then the row and
+// half-wave swaps, which return both directions of the exchange at once.
+template <bool MAX>
+__device__ __forceinline__ uint32_t pick(uint32_t a, uint32_t b) {
+  return MAX ? (a > b ? a : b) : (a < b ? a : b);
 }
-// max over the wave of fp64 values (no NaN): result in lane 63
-__device__ __forceinline__ double wave_max_f64(double x) {
-  x = fmax(x, dpp_f64<0xB1, 0xF>(x));
-  x = fmax(x, dpp_f64<0x4E, 0xF>(x));
-  x = fmax(x, dpp_f64<0x141, 0xF>(x));
-  x = fmax(x, dpp_f64<0x140, 0xF>(x));
-  x = fmax(x, dpp_f64<0x142, 0xA>(x));
-  x = fmax(x, dpp_f64<0x143, 0xC>(x));
-  return x;
+template <bool MAX, int CTRL>
+__device__ __forceinline__ uint32_t dpp_step(uint32_t x) {
+  return pick<MAX>(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, true));
 }
-__device__ __forceinline__ double lane63_f64(double x) {
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t x) {
+  x = dpp_step<MAX, 0xB1>(x);   // quad_perm [1,0,3,2]
+  x = dpp_step<MAX, 0x4E>(x);   // quad_perm [2,3,0,1]
+  x = dpp_step<MAX, 0x141>(x);  // row_half_mirror
+  x = dpp_step<MAX, 0x140>(x);  // row_mirror
+  const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = pick<MAX>(r16[0], r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return pick<MAX>(r32[0], r32[1]);
+}
+// Order-preserving 64-bit key of an fp64 value that is not NaN: a < b exactly when
+// key(a) < key(b), and key(-0) = key(+0) (adding +0 maps -0 to +0 and leaves every other
+// value unchanged).
+__device__ __forceinline__ uint64_t order_key(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x + 0.0);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+// the value of lane i + S in lane i (for the lanes i whose i + S stays in their 2S-lane group):
+// S = 32 and 16 by the half-wave and row swaps, S <= 8 by a row shift
+template <int S>
+__device__ __forceinline__ uint32_t from_lane_plus_u32(uint32_t x) {
+  if constexpr (S == 32) {
+    return __builtin_amdgcn_permlane32_swap(x, x, false, false)[1];
+  } else if constexpr (S == 16) {
+    return __builtin_amdgcn_permlane16_swap(x, x, false, false)[1];
+  } else {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x100 + S, 0xF, 0xF, false);
+  }
+}
+template <int S>
+__device__ __forceinline__ double from_lane_plus(double x) {
   const uint64_t u = __builtin_bit_cast(uint64_t, x);
-  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)u, 63);
-  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+  const uint32_t lo = from_lane_plus_u32<S>((uint32_t)u);
+  const uint32_t hi = from_lane_plus_u32<S>((uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 __device__ __forceinline__ double first_lane_f64(double x) {
@@ -257,11 +280,17 @@ __global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p
   for (int half = E / 2; half >= 1; half >>= 1)
 #pragma unroll
     for (int m = 0; m < half; ++m) a[m] = a[m] + a[m + half];
+  // Cross-lane halvings: lane i adds lane i + s for s = 32, 16, ..., 1 (those below
+  // min(P, 64)); lanes >= s compute values that are never used.  The partner's value comes
+  // from the half-wave and row swaps (s = 32, 16) and row shifts (s <= 8), not through LDS.
   double acc = a[0];
-  for (int stride = (p.P < 64 ? p.P : 64) >> 1; stride >= 1; stride >>= 1) {
-    const double o = __shfl_down(acc, stride);
-    acc = acc + o;  // lanes >= stride compute values that are never used
-  }
+  const int lanes = p.P < 64 ? p.P : 64;
+  if (lanes > 32) acc = acc + from_lane_plus<32>(acc);
+  if (lanes > 16) acc = acc + from_lane_plus<16>(acc);
+  if (lanes > 8) acc = acc + from_lane_plus<8>(acc);
+  if (lanes > 4) acc = acc + from_lane_plus<4>(acc);
+  if (lanes > 2) acc = acc + from_lane_plus<2>(acc);
+  if (lanes > 1) acc = acc + from_lane_plus<1>(acc);
   const double total = first_lane_f64(acc);
   // 4. budget: c = #{ s_j > mean } over U_t, k = ceil(sqrt(c)), clamped
   int c = 0;
@@ -275,44 +304,62 @@ __global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p
   k = min(k, n_elig);
   k = min(k, p.max_seeds);
 
-  // 5. top-k by (score desc, position asc).  Each lane keeps its own best remaining slot bm
-  //    (the smallest m among equal scores, i.e. the smallest position); per round the wave
-  //    takes the largest score, then the smallest (m, lane) holding it, and only the winning
-  //    lane rescans.
-  double bs = 0.0;
+  // 5. top-k by (score desc, position asc), on the order keys of the scores.  Each lane
+  //    keeps its best remaining slot (bk, bm), the smallest m among equal keys, i.e. the
+  //    smallest position.  A round takes the wave maximum of the heads' high words; in the
+  //    usual case one lane holds it and wins.  Otherwise the low words decide, and between
+  //    equal keys the smallest position m * 64 + lane.  The winner drops its slot and every
+  //    lane rescans (only the winner's head can change).
+  uint64_t key[E];
+#pragma unroll
+  for (int m = 0; m < E; ++m) key[m] = order_key(sc[m]);
+  uint64_t bk = 0;  // no real key is 0 (it would be a NaN's)
   int bm = -1;
   auto rescan = [&]() {
+    bk = 0;
     bm = -1;
 #pragma unroll
-    for (int m = 0; m < E; ++m)
-      if (((emask >> m) & 1u) && (bm < 0 || sc[m] > bs)) { bs = sc[m]; bm = m; }
+    for (int m = 0; m < E; ++m) {
+      const bool take = ((emask >> m) & 1u) && key[m] > bk;
+      bk = take ? key[m] : bk;
+      bm = take ? m : bm;
+    }
   };
   rescan();
-  int mine = 0x7fffffff;  // lane t keeps the t-th winner (k <= 32 < 64)
+  uint32_t selm = 0;  // slots of this lane taken as seeds
   for (int t = 0; t < k; ++t) {
-    const double gmax = lane63_f64(wave_max_f64(bm >= 0 ? bs : -INFINITY));
-    const bool cand = bm >= 0 && bs == gmax;
-    int wm = 0;
-    uint64_t wmask = 0;
-#pragma unroll
-    for (int m = 0; m < E; ++m) {
-      if (wmask == 0) {
-        wmask = __builtin_amdgcn_ballot_w64(cand && bm == m);
-        wm = m;
-      }
+    // (the cross-lane reductions are statements of their own, so that every lane takes
+    // part in them; a lane without a slot contributes the identity)
+    const uint32_t hi = bm >= 0 ? (uint32_t)(bk >> 32) : 0u;
+    const uint32_t max_hi = wave_reduce_u32<true>(hi);
+    const bool top_hi = bm >= 0 && hi == max_hi;
+    uint64_t wmask = __builtin_amdgcn_ballot_w64(top_hi);
+    if (__builtin_popcountll(wmask) > 1) {  // uniform
+      const uint32_t lo = top_hi ? (uint32_t)bk : 0u;
+      const uint32_t max_lo = wave_reduce_u32<true>(lo);
+      const bool top = top_hi && lo == max_lo;
+      const uint32_t pos = top ? (uint32_t)(bm * 64 + lane) : 0xFFFFFFFFu;
+      const uint32_t min_pos = wave_reduce_u32<false>(pos);
+      wmask = __builtin_amdgcn_ballot_w64(top && pos == min_pos);
     }
-    const int wl = (int)__builtin_ctzll(wmask);
-    if (lane == wl) {
-      emask &= ~(1u << wm);
-      rescan();
+    if (lane == (int)__builtin_ctzll(wmask)) {
+      selm |= 1u << bm;
+      emask &= ~(1u << bm);
     }
-    if (lane == t) mine = wl + 64 * wm;
+    rescan();
   }
+  // 6. emit ascending: a taken slot's rank is the number of taken positions below it,
+  //    those in lower slots plus those of lower lanes in its own slot
   int32_t* out = p.seed_idx + (int64_t)b * p.max_seeds;
-  if (lane < k) {
-    int rank = 0;
-    for (int u = 0; u < k; ++u) rank += __builtin_amdgcn_readlane(mine, u) < mine;
-    out[rank] = mine + p.pos_offset;
+  int below = 0;
+#pragma unroll
+  for (int m = 0; m < E; ++m) {
+    const bool mine = (selm >> m) & 1u;
+    const uint64_t sm = __builtin_amdgcn_ballot_w64(mine);
+    const int rank = below + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(sm >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)sm, 0u));
+    if (mine) out[rank] = lane + 64 * m + p.pos_offset;
+    below += __builtin_popcountll(sm);
   }
   for (int t = k + lane; t < p.max_seeds; t += 64) out[t] = -1;
   if (lane == 0) p.n_seed[b] = k;

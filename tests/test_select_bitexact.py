@@ -122,3 +122,22 @@ def test_signed_zero_ties(Lr):
     flags = rng.choice([1, 1, 1, 3], (B, Lr)).astype(np.uint8)
     for ms in (4, 32):
         _both(logp, d_in, d_out, flags, ms, 0)
+
+
+@pytest.mark.parametrize("Lr", [64, 256, 1000])
+def test_near_ties_below_the_high_word(Lr):
+    """Scores 2 + k 2^-23 (logp = -1, d_out = 0, d_in = 1 + k 2^-23 in fp32) agree in the upper
+    32 bits of their fp64 encoding and differ only below, while equal k give exact ties: the
+    ranking must use all 64 bits and then the position."""
+    announce(f"select near ties Lr{Lr}")
+    rng = np.random.default_rng(5 + Lr)
+    B = 16
+    k = rng.integers(0, 8, (B, Lr))
+    d_in = (1.0 + k * 2.0 ** -23).astype(np.float32)
+    assert np.array_equal(d_in.astype(np.float64), 1.0 + k * 2.0 ** -23)
+    logp = np.full((B, Lr), -1.0, np.float32)
+    d_out = np.zeros((B, Lr), np.float32)
+    logp[:, ::5] = -0.5   # a lower group, so that the budget is not zero
+    flags = rng.choice([1, 1, 1, 3], (B, Lr)).astype(np.uint8)
+    for ms in (8, 64):
+        _both(logp, d_in, d_out, flags, ms, 0)
