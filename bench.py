@@ -8,7 +8,13 @@ LLaDA-8B layer shape (B=1, H=32, L=1024 = 768 prompt + 256 generated, d=128, bf1
                       positions
 on seeded synthetic inputs already resident in HBM.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload llada|dream|batched]
+  python bench.py [--steps K] [--warmup W] [--workload llada|dream|batched] [--settle-ms T]
+
+Before the W warm-up steps, the timed operation runs back to back, untimed, for T ms of wall
+time (default 100; 0 turns it off).  The GPU raises its clocks over the first tens of
+milliseconds of sustained load: on an MI355X the layer step takes about 31 us in the first
+6 ms and settles at about 27.5 us after about 25 ms.  A decoding loop runs in the settled
+state, so that is the state the timed steps measure.
 
 Profiling helpers (what the committed rocprofv3 summaries were made with):
   --only attn|select   time only that kernel in the step
@@ -64,11 +70,31 @@ def measured_traffic(workload: str):
     return int(m.group(1))
 
 
+def settle_clocks(fn, ms: float) -> int:
+    """Run `fn` back to back for `ms` milliseconds of wall time, untimed, so that the timed
+    launches see the clocks of sustained load; returns how many calls it made."""
+    import torch
+
+    n = 0
+    t_end = time.perf_counter() + ms * 1e-3
+    while time.perf_counter() < t_end:
+        for _ in range(16):
+            fn()
+        torch.cuda.synchronize()
+        n += 16
+    return n
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="untimed back-to-back run before the warm-up steps (clock ramp)")
+    ap.add_argument("--ramp-windows", type=int, default=0,
+                    help="first time N consecutive windows of 200 steps (the clock ramp) and "
+                         "report them as ramp_us_per_step")
     ap.add_argument("--workload", default="llada", choices=["llada", "dream", "batched", "step", "loop", "block"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--only", choices=["attn", "select"], default=None)
@@ -164,6 +190,23 @@ def main() -> int:
 
     do_attn = args.only in (None, "attn")
     do_sel = args.only in (None, "select")
+
+    def one_step():
+        if do_attn:
+            attn()
+        if do_sel:
+            select()
+
+    ramp = []
+    for _ in range(args.ramp_windows):  # the clock ramp, window by window, from a cold start
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r0.record(stream)
+        for _ in range(200):
+            one_step()
+        r1.record(stream)
+        torch.cuda.synchronize()
+        ramp.append(round(r0.elapsed_time(r1) * 1e3 / 200, 3))
+    settle_clocks(one_step, args.settle_ms)
     for _ in range(args.warmup):
         if do_attn:
             attn()
@@ -245,6 +288,8 @@ def main() -> int:
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
+        "settle_ms": args.settle_ms,
+        **({"ramp_us_per_step": ramp} if ramp else {}),
         "ms_per_step": round(ms_per_step, 5),
         "us_per_layer_step": round(ms_per_step * 1e3, 3),
         "pct_bf16_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
@@ -276,7 +321,7 @@ def main() -> int:
         },
     }
     if not args.no_phase_timing:
-        ph = phase_leg(args.workload)
+        ph = phase_leg(args.workload, args.settle_ms)
         if ph is not None:
             rec["sclk_ghz_under_load"] = ph["sclk_ghz_median"]
             rec["phase_cycles_median"] = ph["cycles_median"]
@@ -286,14 +331,14 @@ def main() -> int:
     return 0
 
 
-def phase_leg(workload: str):
+def phase_leg(workload: str, settle_ms: float):
     """The timing build of the attention kernel, run once after warm-up in a child process
     (`--phase-timing`): the shader clock under load and the per-phase cycle medians.  None
     (with a note on stderr) if that run fails."""
     import subprocess
 
     cmd = [sys.executable, os.path.abspath(__file__), "--phase-timing", "--workload", workload,
-           "--warmup", "5"]
+           "--warmup", "5", "--settle-ms", str(settle_ms)]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
     if r.returncode != 0 or not lines:
@@ -384,6 +429,7 @@ def bench_producer(args, dev, stream) -> int:
         cfg = {"workload": f"LLaDA-8B last layer, generated block: B={c.B} Hq={c.Hq} "
                            f"Lr={a['Lr']} of L={c.L}, d={c.d} bf16"}
         bound, unit, peak = "latency", "TFLOP/s", PEAK_BF16_TFLOPS
+    settle_clocks(run, args.settle_ms)
     for _ in range(args.warmup):
         if run() != 0:
             raise RuntimeError(f"{args.kernel} launch rejected")
@@ -607,6 +653,7 @@ def bench_phase_timing(args, dev, stream) -> int:
                                    "n_seed")}
     attn = cover.PreparedAttn(t["q"], t["k_live"], t["v_live"], t["k_cache"], t["v_cache"],
                               t["seed_idx"], t["n_seed"], stream=stream)
+    settle_clocks(attn, args.settle_ms)
     for _ in range(args.warmup):
         attn()
     torch.cuda.synchronize()
@@ -700,6 +747,7 @@ def bench_block_phase_timing(args, dev, stream) -> int:
         qb = q[:, :, q_off:q_off + Lq].contiguous()
         call = cover.PreparedRect(qb, kl, vl, kc, vc, q_off, si if seeded else None,
                                   ns if seeded else None, n_split=1, stream=stream)
+        settle_clocks(call, args.settle_ms)
         for _ in range(max(1, args.warmup)):
             call()
         torch.cuda.synchronize()
@@ -757,6 +805,7 @@ def bench_block(args, dev, stream) -> int:
         # Python's per-call overhead (about 12 us, near the kernel's own time)
         call = cover.PreparedRect(qb, kl, vl, kc, vc, q_off, si, ns, stream=stream)
         n = call.n_split
+        settle_clocks(call, args.settle_ms)
         for _ in range(max(1, args.warmup)):
             call()
         torch.cuda.synchronize()
