@@ -342,7 +342,8 @@ __global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p
       const uint32_t min_pos = wave_reduce_u32<false>(pos);
       wmask = __builtin_amdgcn_ballot_w64(top && pos == min_pos);
     }
-    if (lane == (int)__builtin_ctzll(wmask)) {
+    // (no winner only if the data contract is broken, e.g. a NaN score: no lane takes one)
+    if (wmask != 0 && lane == (int)__builtin_ctzll(wmask)) {
       selm |= 1u << bm;
       emask &= ~(1u << bm);
     }
@@ -361,6 +362,9 @@ __global__ __launch_bounds__(64) void cover_select_wave_kernel(const SelParams p
     if (mine) out[rank] = lane + 64 * m + p.pos_offset;
     below += __builtin_popcountll(sm);
   }
+  // below == k for valid inputs; the list is filled and counted from what was emitted, so
+  // that no slot is left unwritten otherwise
+  k = below;
   for (int t = k + lane; t < p.max_seeds; t += 64) out[t] = -1;
   if (lane == 0) p.n_seed[b] = k;
 }
