@@ -70,17 +70,20 @@ def measured_traffic(workload: str):
     return int(m.group(1))
 
 
-def settle_clocks(fn, ms: float) -> int:
+def settle_clocks(fn, ms: float, sync=None) -> int:
     """Run `fn` back to back for `ms` milliseconds of wall time, untimed, so that the timed
-    launches see the clocks of sustained load; returns how many calls it made."""
-    import torch
+    launches see the clocks of sustained load; returns how many calls it made.  `sync` waits
+    for the queued work (the device by default), every 16 calls."""
+    if sync is None:
+        import torch
 
+        sync = torch.cuda.synchronize
     n = 0
     t_end = time.perf_counter() + ms * 1e-3
     while time.perf_counter() < t_end:
         for _ in range(16):
             fn()
-        torch.cuda.synchronize()
+        sync()
         n += 16
     return n
 

@@ -1,6 +1,6 @@
 """Host-side checks of bench.py (no GPU): the multi-GPU request is refused with a message,
 and the HBM traffic figure is taken from the committed profile only while the kernel source
-it was measured on is unchanged."""
+it was measured on is unchanged; the clock-settle run lasts as long as asked."""
 import os
 import re
 import subprocess
@@ -35,3 +35,18 @@ def test_traffic_figure_tracks_the_kernel_source():
         else:
             assert got is None
     assert bench.measured_traffic("no-such-workload") is None
+
+
+def test_clock_settle_runs_for_the_requested_time():
+    """The settle run before the warm-up calls the step for at least the requested wall time,
+    waiting for the queued work every 16 calls, and not at all for 0 ms."""
+    import time
+
+    calls, syncs = [], []
+    assert bench.settle_clocks(lambda: calls.append(1), 0.0, sync=lambda: syncs.append(1)) == 0
+    assert not calls and not syncs
+    t0 = time.perf_counter()
+    n = bench.settle_clocks(lambda: calls.append(1), 20.0, sync=lambda: syncs.append(1))
+    assert time.perf_counter() - t0 >= 0.020
+    assert n == len(calls) and n >= 16 and n % 16 == 0
+    assert len(syncs) == n // 16
